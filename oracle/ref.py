@@ -1,0 +1,193 @@
+"""CPU oracle for one mixed prefill+decode step over a paged KV cache.
+
+TEST INFRASTRUCTURE ONLY.  The tests, the smoke check and the benchmark's
+CPU-baseline leg call this module; the library and its Python binding never
+import it, and it imports nothing of theirs.  It is plain, slow numpy in
+float64.
+
+What the step computes.  The paper (section 2.1) describes prefill as
+materialising the KV cache of the input tokens and decode as producing one
+token per running sequence while re-reading an expanding KV cache; section 4.4
+has the decode node reuse a resident (radix-cached) prefix and process the
+remaining prompt tokens; section 5 co-batches those prefill chunks with the
+running decode rows in one mixed batch.  The paper never writes the attention
+formula, so the oracle is the textbook definition of scaled dot-product
+softmax attention with these readings of what the paper leaves unsaid:
+
+* a sequence with KV length ``L`` (after the append) and ``C`` new tokens has
+  a cached prefix ``P = L - C``; new token ``i`` sits at logical position
+  ``P + i`` and sees keys ``0 .. P + i`` inclusive (bottom-right causal);
+  a decode row is the case ``C = 1``;
+* query head ``h`` reads KV head ``h // G`` with ``G = Hq / Hkv`` (contiguous
+  groups);
+* the softmax scale is a parameter (the tests use ``1 / sqrt(head_dim)``);
+* the step appends first and attends second, so the oracle gathers each
+  sequence's keys from the pool as it was *before* the append, plus this
+  step's ``k_new`` / ``v_new`` rows for positions ``P .. L - 1``.
+
+Cache layout read here (the library header's definition), with
+``X = 16 / element_bytes``: K element (block b, head h, slot t, dim i) is at
+``[b][h][i // X][t][i % X]``; V element (b, h, t, i) is at ``[b][h][i][t]``.
+bf16 values arrive as their 16-bit patterns.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+ELEM_BYTES = {"bf16": 2, "f32": 4}
+
+
+def decode_raw(raw: np.ndarray, dtype: str) -> np.ndarray:
+    """Raw storage -> float64.  A bf16 pattern is the top half of a float32."""
+    if dtype == "bf16":
+        u = np.ascontiguousarray(raw, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+        return u.view(np.float32).astype(np.float64)
+    if dtype == "f32":
+        return np.asarray(raw, dtype=np.float32).astype(np.float64)
+    raise ValueError(dtype)
+
+
+def _x(dtype: str) -> int:
+    return 16 // ELEM_BYTES[dtype]
+
+
+def gather_kv(k_cache, v_cache, block_row, n_tokens, num_kv_heads, head_dim, block_size, dtype):
+    """Logical positions 0 .. n_tokens-1 of one sequence, as float64
+    ``[n_tokens, Hkv, d]`` arrays: position p is slot ``p % bs`` of physical
+    block ``block_row[p // bs]``."""
+    if n_tokens == 0:
+        z = np.zeros((0, num_kv_heads, head_dim))
+        return z, z.copy()
+    x = _x(dtype)
+    nb = -(-n_tokens // block_size)
+    blocks = np.asarray(block_row[:nb], dtype=np.int64)
+    kb = k_cache.reshape(-1, num_kv_heads, head_dim // x, block_size, x)[blocks]
+    vb = v_cache.reshape(-1, num_kv_heads, head_dim, block_size)[blocks]
+    # [nb, H, d/X, bs, X] -> [nb, bs, H, d/X, X] -> [nb*bs, H, d]
+    k = decode_raw(kb, dtype).transpose(0, 3, 1, 2, 4).reshape(nb * block_size, num_kv_heads, head_dim)
+    # [nb, H, d, bs] -> [nb, bs, H, d]
+    v = decode_raw(vb, dtype).transpose(0, 3, 1, 2).reshape(nb * block_size, num_kv_heads, head_dim)
+    return k[:n_tokens], v[:n_tokens]
+
+
+def softmax_attention(q, k, v, scale, visible):
+    """Scaled dot-product attention for one head.
+
+    q [n, d], k [L, d], v [L, d] float64; ``visible`` [n, L] bool says which
+    keys each query row may attend.  Every row must see at least one key.
+    Returns (o [n, d], lse [n]) with lse the natural log of the softmax
+    denominator of the scaled scores.  The row maximum is subtracted before
+    exponentiating; the masked scores are removed by selection."""
+    # Contiguous operands, so the result depends on the values only and not
+    # on the strides a gather happened to produce.
+    q, k, v = (np.ascontiguousarray(a, dtype=np.float64) for a in (q, k, v))
+    s = scale * (q @ k.T)
+    s = np.where(visible, s, -np.inf)
+    m = s.max(axis=1, keepdims=True)
+    e = np.exp(s - m)
+    l = e.sum(axis=1, keepdims=True)
+    o = (e @ v) / l
+    return o, (m + np.log(l))[:, 0]
+
+
+def lse_merge(parts):
+    """Combine attention results over disjoint key sets.
+
+    ``parts`` is a list of (o [n, d], lse [n]).  Softmax over the union of the
+    key sets re-weights each part by its share of the total denominator,
+    exp(lse_j - lse), with lse = log(sum_j exp(lse_j))."""
+    lses = np.stack([p[1] for p in parts])  # [J, n]
+    top = lses.max(axis=0)
+    w = np.exp(lses - top)  # [J, n]
+    total = w.sum(axis=0)
+    o = sum(w[j][:, None] * parts[j][0] for j in range(len(parts))) / total[:, None]
+    return o, top + np.log(total)
+
+
+def sequence_attention(q_rows, k, v, prefix, scale, num_kv_heads, row_tile=512):
+    """All query heads of one sequence.
+
+    q_rows [C, Hq, d]; k, v [L, Hkv, d] with L = prefix + C.  Row i sits at
+    position prefix + i and sees keys 0 .. prefix + i."""
+    c, hq, d = q_rows.shape
+    big_l = k.shape[0]
+    g = hq // num_kv_heads
+    o = np.empty((c, hq, d))
+    lse = np.empty((c, hq))
+    keys = np.arange(big_l)
+    for r0 in range(0, c, row_tile):
+        r1 = min(c, r0 + row_tile)
+        visible = keys[None, :] <= (prefix + np.arange(r0, r1))[:, None]
+        for h in range(hq):
+            kv = h // g
+            o[r0:r1, h], lse[r0:r1, h] = softmax_attention(
+                q_rows[r0:r1, h], k[:, kv], v[:, kv], scale, visible
+            )
+    return o, lse
+
+
+def attention_reference(
+    q,
+    k_cache,
+    v_cache,
+    k_new,
+    v_new,
+    block_tables,
+    seq_lens,
+    query_start_loc,
+    scale,
+    num_kv_heads,
+    block_size,
+    dtype,
+    seqs=None,
+):
+    """Outputs of one mixed step.
+
+    Raw inputs in the library's layouts; the caches are the pool *before* the
+    step's append.  Returns (out [T, Hq, d], lse [T, Hq]) float64; rows of
+    sequences not in ``seqs`` (default: all) are NaN."""
+    qf = decode_raw(q, dtype)
+    t, hq, d = qf.shape
+    out = np.full((t, hq, d), np.nan)
+    lse = np.full((t, hq), np.nan)
+    seq_lens = np.asarray(seq_lens)
+    qsl = np.asarray(query_start_loc)
+    todo = range(len(seq_lens)) if seqs is None else seqs
+    for s in todo:
+        t0, t1 = int(qsl[s]), int(qsl[s + 1])
+        c = t1 - t0
+        if c == 0:
+            continue
+        big_l = int(seq_lens[s])
+        prefix = big_l - c
+        kp, vp = gather_kv(k_cache, v_cache, block_tables[s], prefix, num_kv_heads, d, block_size, dtype)
+        k = np.concatenate([kp, decode_raw(k_new[t0:t1], dtype)], axis=0)
+        v = np.concatenate([vp, decode_raw(v_new[t0:t1], dtype)], axis=0)
+        out[t0:t1], lse[t0:t1] = sequence_attention(qf[t0:t1], k, v, prefix, scale, num_kv_heads)
+    return out, lse
+
+
+def append_reference(k_cache, v_cache, k_new, v_new, block_tables, seq_lens, query_start_loc, block_size, dtype):
+    """The pool after the step's append, as raw copies of the inputs.
+
+    Token i of sequence s goes to logical position P_s + i, i.e. slot
+    ``(P_s + i) % bs`` of block ``block_tables[s][(P_s + i) // bs]``; its bits
+    are copied unchanged.  Nothing else in the pool changes."""
+    x = _x(dtype)
+    kc = k_cache.copy()
+    vc = v_cache.copy()
+    t, hkv, d = k_new.shape
+    k5 = kc.reshape(-1, hkv, d // x, block_size, x)
+    v4 = vc.reshape(-1, hkv, d, block_size)
+    qsl = np.asarray(query_start_loc)
+    for s in range(len(seq_lens)):
+        t0, t1 = int(qsl[s]), int(qsl[s + 1])
+        if t1 == t0:
+            continue
+        pos = int(seq_lens[s]) - (t1 - t0) + np.arange(t1 - t0)
+        blk = np.asarray(block_tables[s])[pos // block_size]
+        slot = pos % block_size
+        k5[blk, :, :, slot, :] = k_new[t0:t1].reshape(t1 - t0, hkv, d // x, x)
+        v4[blk, :, :, slot] = v_new[t0:t1]
+    return kc, vc

@@ -1,0 +1,89 @@
+"""Planted mistakes in the oracle (CPU only) must each break at least one pin.
+
+Each mutant replaces one oracle function with a plausible wrong variant -- a
+shifted causal diagonal, the interleaved head mapping, a dropped scale, a
+transposed cache layout, a dropped term of the log-sum-exp -- and the test
+asserts that the pins of ``test_oracle_pins`` reject it.
+"""
+
+import numpy as np
+import pytest
+
+import test_oracle_pins as pins
+from oracle import ref
+
+
+def _seq_attn_factory(visible_fn=None, head_map=None, scale_override=None):
+    def seq_attn(q_rows, k, v, prefix, scale, num_kv_heads, row_tile=512):
+        c, hq, d = q_rows.shape
+        big_l = k.shape[0]
+        g = hq // num_kv_heads
+        o = np.empty((c, hq, d))
+        lse = np.empty((c, hq))
+        keys = np.arange(big_l)
+        rows = np.arange(c)
+        vis = visible_fn(keys, rows, prefix) if visible_fn else keys[None] <= (prefix + rows)[:, None]
+        vis = vis | (keys[None] == 0)  # keep every row non-empty
+        for h in range(hq):
+            kv = head_map(h, g, num_kv_heads) if head_map else h // g
+            o[:, h], lse[:, h] = ref.softmax_attention(
+                q_rows[:, h], k[:, kv], v[:, kv], scale if scale_override is None else scale_override, vis)
+        return o, lse
+    return seq_attn
+
+
+def _bad_lse(q, k, v, scale, visible):
+    o, lse = _good_softmax(q, k, v, scale, visible)
+    s = np.where(visible, scale * (q @ k.T), -np.inf)
+    return o, lse - s.max(axis=1)  # drops the maximum from the log-sum-exp
+
+
+_good_softmax = ref.softmax_attention
+
+
+def _transposed_gather(k_cache, v_cache, block_row, n_tokens, num_kv_heads, head_dim, block_size, dtype):
+    if n_tokens == 0:
+        z = np.zeros((0, num_kv_heads, head_dim))
+        return z, z.copy()
+    nb = -(-n_tokens // block_size)
+    blocks = np.asarray(block_row[:nb], dtype=np.int64)
+    # wrong: reads K as [b][h][t][d] (the "natural" layout) instead of the header's
+    kb = ref.decode_raw(k_cache.reshape(-1, num_kv_heads, block_size, head_dim)[blocks], dtype)
+    vb = ref.decode_raw(v_cache.reshape(-1, num_kv_heads, head_dim, block_size)[blocks], dtype)
+    k = kb.transpose(0, 2, 1, 3).reshape(-1, num_kv_heads, head_dim)
+    v = vb.transpose(0, 3, 1, 2).reshape(-1, num_kv_heads, head_dim)
+    return k[:n_tokens], v[:n_tokens]
+
+
+MUTANTS = {
+    "top_left_causal": ("sequence_attention", _seq_attn_factory(
+        visible_fn=lambda keys, rows, prefix: keys[None] <= rows[:, None])),
+    "exclusive_diagonal": ("sequence_attention", _seq_attn_factory(
+        visible_fn=lambda keys, rows, prefix: keys[None] < (prefix + rows)[:, None])),
+    "interleaved_heads": ("sequence_attention", _seq_attn_factory(
+        head_map=lambda h, g, hkv: h % hkv)),
+    "dropped_scale": ("sequence_attention", _seq_attn_factory(scale_override=1.0)),
+    "lse_without_max": ("softmax_attention", _bad_lse),
+    "natural_k_layout": ("gather_kv", _transposed_gather),
+}
+
+PIN_TESTS = [
+    lambda: pins.test_golden_hand_worked(),
+    lambda: pins.test_brute_force("f32", 0),
+    lambda: pins.test_brute_force("bf16", 1),
+    lambda: pins.test_block_size_invariance_and_sdpa("f32"),
+    lambda: pins.test_zero_query_gives_running_mean(),
+]
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, monkeypatch):
+    attr, fn = MUTANTS[name]
+    monkeypatch.setattr(ref, attr, fn)
+    caught = 0
+    for t in PIN_TESTS:
+        try:
+            t()
+        except AssertionError:
+            caught += 1
+    assert caught > 0, f"no pin rejects the mutant {name}"

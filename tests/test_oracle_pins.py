@@ -1,0 +1,419 @@
+"""Pins for the CPU oracle: each checks it against something other than itself.
+
+* a hand-worked closed-form fixture (tests/golden/hand_worked.txt);
+* brute force on tiny inputs, reading the pool through the header's flat
+  offset formula and exponentiating without subtracting the maximum;
+* closed forms: context length 1 returns V exactly, Q = 0 gives the running
+  mean of V, identical keys give the mean of V, a dominant key returns its V;
+* invariances: block-table permutation, block size, paged vs contiguous;
+* a library special case: torch float64 scaled_dot_product_attention with an
+  explicit bottom-right mask and repeat_interleave for grouped heads;
+* the split/merge identity of the softmax denominators;
+* row independence of a mixed batch;
+* the append: new bits land at their slots and nothing else changes.
+"""
+
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import ref
+from workloads import HeadSpec, SeqSpec, make_batch
+from workloads.gen import bf16_bits_from_f32, k_cache_shape, v_cache_shape
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_worked.txt")
+
+
+def run_oracle(b, seqs=None):
+    return ref.attention_reference(
+        b.q, b.k_cache, b.v_cache, b.k_new, b.v_new, b.block_tables, b.seq_lens,
+        b.query_start_loc, b.scale, b.heads.num_kv_heads, b.heads.block_size, b.dtype, seqs=seqs,
+    )
+
+
+# ----------------------------------------------------------------------------
+# hand-worked fixture
+
+
+def _golden_rows():
+    rows = []
+    with open(GOLDEN) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            p = line.split()
+            rows.append((p[0], int(p[1]), int(p[2]), [Fraction(x) for x in p[3:7]], int(p[7])))
+    return rows
+
+
+def _f32_pool(nb, hkv, d, bs):
+    k = np.full(k_cache_shape(nb, HeadSpec(hkv, hkv, d, bs), "f32"), np.nan, dtype=np.float32)
+    v = np.full(v_cache_shape(nb, HeadSpec(hkv, hkv, d, bs), "f32"), np.nan, dtype=np.float32)
+    return k, v
+
+
+def _put_k(kc, b, h, t, vec):
+    # header formula: K element (b, h, t, i) at [b][h][i // X][t][i % X], X = 4 for f32
+    for i, val in enumerate(vec):
+        kc[b, h, i // 4, t, i % 4] = val
+
+
+def _put_v(vc, b, h, t, vec):
+    for i, val in enumerate(vec):
+        vc[b, h, i, t] = val
+
+
+def test_golden_hand_worked():
+    d, bs = 4, 2
+    e = np.eye(4, dtype=np.float32)
+    kvec = [np.array([j, 0, 0, 0], dtype=np.float32) for j in range(4)]
+    scale = math.log(2.0)
+    got = {}
+    # case A: P = 0, chunk of 3, one head; everything arrives as new tokens.
+    kc, vc = _f32_pool(2, 1, d, bs)
+    q = np.array([[[1, 0, 0, 0]]] * 3, dtype=np.float32)
+    kn = np.stack(kvec[:3])[:, None, :]
+    vn = e[:3][:, None, :]
+    o, lse = ref.attention_reference(
+        q, kc, vc, kn, vn, np.array([[0, 1]], np.int32), np.array([3], np.int32),
+        np.array([0, 3], np.int32), scale, 1, bs, "f32")
+    for r in range(3):
+        got[("A", r, 0)] = (o[r, 0], lse[r, 0])
+    # case B: P = 2 cached in block 1, chunk of 2 new tokens into block 0, Hq=2, Hkv=1.
+    kc, vc = _f32_pool(2, 1, d, bs)
+    for j in range(2):
+        _put_k(kc, 1, 0, j, kvec[j])
+        _put_v(vc, 1, 0, j, e[j])
+    q = np.array([[[1, 0, 0, 0], [0, 0, 0, 0]]] * 2, dtype=np.float32)
+    kn = np.stack(kvec[2:4])[:, None, :]
+    vn = e[2:4][:, None, :]
+    o, lse = ref.attention_reference(
+        q, kc, vc, kn, vn, np.array([[1, 0]], np.int32), np.array([4], np.int32),
+        np.array([0, 2], np.int32), scale, 1, bs, "f32")
+    for r in range(2):
+        for h in range(2):
+            got[("B", r, h)] = (o[r, h], lse[r, h])
+    rows = _golden_rows()
+    assert len(rows) == 7
+    for case, r, h, ofr, lse_arg in rows:
+        o_got, lse_got = got[(case, r, h)]
+        np.testing.assert_allclose(o_got, [float(x) for x in ofr], rtol=0, atol=1e-14)
+        assert abs(lse_got - math.log(lse_arg)) < 1e-13
+
+
+# ----------------------------------------------------------------------------
+# brute force
+
+
+def _flat_k(b, h, t, i, hkv, d, bs, x):
+    return ((((b * hkv + h) * (d // x) + i // x) * bs + t) * x) + i % x
+
+
+def _flat_v(b, h, t, i, hkv, d, bs):
+    return ((b * hkv + h) * d + i) * bs + t
+
+
+def _brute(b):
+    """Double loop; exp without max subtraction; pool read by flat offsets."""
+    hq, hkv, d, bs = b.heads.num_q_heads, b.heads.num_kv_heads, b.heads.head_dim, b.heads.block_size
+    x = 16 // (2 if b.dtype == "bf16" else 4)
+    qv = ref.decode_raw(b.q, b.dtype)
+    kn = ref.decode_raw(b.k_new, b.dtype)
+    vn = ref.decode_raw(b.v_new, b.dtype)
+    kflat = ref.decode_raw(b.k_cache, b.dtype).ravel()
+    vflat = ref.decode_raw(b.v_cache, b.dtype).ravel()
+    g = hq // hkv
+    out = np.zeros(qv.shape)
+    lse = np.zeros(qv.shape[:2])
+    for s in range(b.num_seqs):
+        t0, t1 = int(b.query_start_loc[s]), int(b.query_start_loc[s + 1])
+        L = int(b.seq_lens[s])
+        P = L - (t1 - t0)
+        for i in range(t1 - t0):
+            for h in range(hq):
+                kh = h // g
+                den = 0.0
+                num = [0.0] * d
+                for j in range(P + i + 1):
+                    if j < P:
+                        blk = int(b.block_tables[s, j // bs])
+                        kj = [kflat[_flat_k(blk, kh, j % bs, c, hkv, d, bs, x)] for c in range(d)]
+                        vj = [vflat[_flat_v(blk, kh, j % bs, c, hkv, d, bs)] for c in range(d)]
+                    else:
+                        kj = list(kn[t0 + j - P, kh])
+                        vj = list(vn[t0 + j - P, kh])
+                    sc = b.scale * sum(qv[t0 + i, h, c] * kj[c] for c in range(d))
+                    w = math.exp(sc)
+                    den += w
+                    for c in range(d):
+                        num[c] += w * vj[c]
+                out[t0 + i, h] = [n / den for n in num]
+                lse[t0 + i, h] = math.log(den)
+    return out, lse
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("seed", [0, 1])
+def test_brute_force(dtype, seed):
+    specs = [SeqSpec(5, 1), SeqSpec(9, 3), SeqSpec(1, 1), SeqSpec(4, 4), SeqSpec(7, 0), SeqSpec(12, 2)]
+    b = make_batch(specs, HeadSpec(4, 2, 8, 4), dtype, seed)
+    o, lse = run_oracle(b)
+    ob, lb = _brute(b)
+    np.testing.assert_allclose(o, ob, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse, lb, rtol=0, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# closed forms
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_context_one_returns_v_exactly(dtype):
+    specs = [SeqSpec(1, 1), SeqSpec(1, 1), SeqSpec(1, 1)]
+    b = make_batch(specs, HeadSpec(8, 2, 16, 16), dtype, 3)
+    o, lse = run_oracle(b)
+    v = ref.decode_raw(b.v_new, dtype)
+    g = 4
+    for h in range(8):
+        assert np.array_equal(o[:, h], v[:, h // g])
+    # one key: the denominator is exp(score) itself, so lse is the scaled score
+    qv = ref.decode_raw(b.q, dtype)
+    kv = ref.decode_raw(b.k_new, dtype)
+    for h in range(8):
+        np.testing.assert_allclose(lse[:, h], b.scale * (qv[:, h] * kv[:, h // g]).sum(-1), rtol=0, atol=1e-14)
+
+
+def test_zero_query_gives_running_mean():
+    specs = [SeqSpec(40, 7), SeqSpec(9, 9), SeqSpec(30, 1)]
+    b = make_batch(specs, HeadSpec(4, 4, 16, 8), "f32", 4)
+    b.q[:] = 0
+    o, lse = run_oracle(b)
+    for s in range(3):
+        t0, t1 = int(b.query_start_loc[s]), int(b.query_start_loc[s + 1])
+        L = int(b.seq_lens[s])
+        P = L - (t1 - t0)
+        _, vp = ref.gather_kv(b.k_cache, b.v_cache, b.block_tables[s], P, 4, 16, 8, "f32")
+        v = np.concatenate([vp, b.v_new[t0:t1].astype(np.float64)])
+        cm = np.cumsum(v, axis=0) / np.arange(1, L + 1)[:, None, None]
+        np.testing.assert_allclose(o[t0:t1], cm[P:L], rtol=0, atol=1e-13)
+        np.testing.assert_allclose(lse[t0:t1], np.log(np.arange(P + 1, L + 1))[:, None] * np.ones(4), atol=1e-13)
+
+
+def test_identical_keys_give_mean():
+    specs = [SeqSpec(33, 1), SeqSpec(20, 5)]
+    b = make_batch(specs, HeadSpec(4, 2, 8, 16), "f32", 5, nan_fill=False)
+    b.k_cache[:] = 0.5
+    b.k_new[:] = 0.5
+    o, _ = run_oracle(b)
+    for s in range(2):
+        t0, t1 = int(b.query_start_loc[s]), int(b.query_start_loc[s + 1])
+        L = int(b.seq_lens[s])
+        P = L - (t1 - t0)
+        _, vp = ref.gather_kv(b.k_cache, b.v_cache, b.block_tables[s], P, 2, 8, 16, "f32")
+        v = np.concatenate([vp, b.v_new[t0:t1].astype(np.float64)])
+        for i in range(t1 - t0):
+            mean = v[: P + i + 1].mean(axis=0)  # [Hkv, d]
+            for h in range(4):
+                np.testing.assert_allclose(o[t0 + i, h], mean[h // 2], rtol=0, atol=1e-13)
+
+
+def test_dominant_key_returns_its_value():
+    # Orthogonal keys; q = alpha * k_t makes key t's weight 1 - O(L e^{-alpha}).
+    d, L, t = 16, 12, 7
+    specs = [SeqSpec(L, 1)]
+    b = make_batch(specs, HeadSpec(1, 1, d, 4), "f32", 6, scale=1.0)
+    keys = np.eye(d, dtype=np.float32)[:L]
+    for j in range(L - 1):
+        blk = b.block_tables[0, j // 4]
+        _put_k(b.k_cache, blk, 0, j % 4, keys[j])
+    b.k_new[0, 0] = keys[L - 1]
+    for alpha in (20.0, 40.0):
+        b.q[0, 0] = alpha * keys[t]
+        o, _ = run_oracle(b)
+        _, v = ref.gather_kv(b.k_cache, b.v_cache, b.block_tables[0], L - 1, 1, d, 4, "f32")
+        assert np.abs(o[0, 0] - v[t, 0]).max() < L * math.exp(-alpha) * 10
+
+
+# ----------------------------------------------------------------------------
+# invariances
+
+
+def _permute_pool(b, rng):
+    """Same logical contents, physical blocks relabelled by a permutation."""
+    perm = rng.permutation(b.num_blocks)  # new id of old block i is perm[i]
+    inv = np.argsort(perm)
+    kc = b.k_cache[inv].copy()
+    vc = b.v_cache[inv].copy()
+    bt = np.where(b.block_tables >= 0, perm[np.maximum(b.block_tables, 0)], -1).astype(np.int32)
+    return kc, vc, bt
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_block_permutation_invariance(dtype):
+    specs = [SeqSpec(70, 1), SeqSpec(50, 13), SeqSpec(17, 1), SeqSpec(64, 64)]
+    b = make_batch(specs, HeadSpec(4, 2, 16, 16), dtype, 7)
+    o1, l1 = run_oracle(b)
+    kc, vc, bt = _permute_pool(b, np.random.default_rng(1))
+    o2, l2 = ref.attention_reference(b.q, kc, vc, b.k_new, b.v_new, bt, b.seq_lens, b.query_start_loc,
+                                     b.scale, 2, 16, dtype)
+    assert np.array_equal(o1, o2) and np.array_equal(l1, l2)
+
+
+def _logical_to_pool(kl, vl, bs, dtype, rng):
+    """Scatter contiguous per-sequence KV [L, H, d] into a shuffled pool of
+    block size bs (test-side writer using the header layout)."""
+    hkv, d = kl[0].shape[1], kl[0].shape[2]
+    x = 16 // (2 if dtype == "bf16" else 4)
+    nbs = [-(-k.shape[0] // bs) for k in kl]
+    nb = sum(nbs)
+    perm = rng.permutation(nb)
+    raw = np.uint16 if dtype == "bf16" else np.float32
+    kc = np.zeros((nb, hkv, d // x, bs, x), dtype=raw)
+    vc = np.zeros((nb, hkv, d, bs), dtype=raw)
+    bt = np.full((len(kl), max(nbs)), -1, np.int32)
+    off = 0
+    for s, (k, v) in enumerate(zip(kl, vl)):
+        for p in range(k.shape[0]):
+            blk = perm[off + p // bs]
+            bt[s, p // bs] = blk
+            kc[blk, :, :, p % bs, :] = k[p].reshape(hkv, d // x, x)
+            vc[blk, :, :, p % bs] = v[p]
+        off += nbs[s]
+    return kc, vc, bt
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_block_size_invariance_and_sdpa(dtype):
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(8)
+    hq, hkv, d = 8, 2, 16
+    ctx = [37, 1, 64, 29]
+    qlen = [5, 1, 64, 1]
+    raw = np.uint16 if dtype == "bf16" else np.float32
+
+    def draw(shape):
+        v = rng.standard_normal(shape, dtype=np.float32)
+        return bf16_bits_from_f32(v) if dtype == "bf16" else v
+
+    kl = [draw((c, hkv, d)) for c in ctx]
+    vl = [draw((c, hkv, d)) for c in ctx]
+    q = draw((sum(qlen), hq, d))
+    qsl = np.concatenate([[0], np.cumsum(qlen)]).astype(np.int32)
+    seq_lens = np.array(ctx, np.int32)
+    k_new = np.concatenate([k[c - n:] for k, c, n in zip(kl, ctx, qlen)]).astype(raw)
+    v_new = np.concatenate([v[c - n:] for v, c, n in zip(vl, ctx, qlen)]).astype(raw)
+    outs = []
+    for bs in (1, 8, 16, 32):
+        kc, vc, bt = _logical_to_pool(kl, vl, bs, dtype, rng)
+        outs.append(ref.attention_reference(q, kc, vc, k_new, v_new, bt, seq_lens, qsl, 0.25, hkv, bs, dtype))
+    for o, l in outs[1:]:
+        assert np.array_equal(o, outs[0][0]) and np.array_equal(l, outs[0][1])
+    # Library special case: per sequence, torch fp64 SDPA on the contiguous
+    # arrays with an explicit bottom-right mask and repeat_interleave groups.
+    o0 = outs[0][0]
+    for s in range(len(ctx)):
+        t0, t1 = qsl[s], qsl[s + 1]
+        c, n = ctx[s], qlen[s]
+        qt = torch.from_numpy(ref.decode_raw(q[t0:t1], dtype)).permute(1, 0, 2)  # [Hq, n, d]
+        kt = torch.from_numpy(ref.decode_raw(kl[s], dtype)).permute(1, 0, 2).repeat_interleave(hq // hkv, 0)
+        vt = torch.from_numpy(ref.decode_raw(vl[s], dtype)).permute(1, 0, 2).repeat_interleave(hq // hkv, 0)
+        mask = torch.arange(c)[None, :] <= (c - n + torch.arange(n))[:, None]
+        st = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, attn_mask=mask, scale=0.25)
+        np.testing.assert_allclose(o0[t0:t1], st.permute(1, 0, 2).numpy(), rtol=0, atol=1e-12)
+
+
+def test_split_merge_identity():
+    rng = np.random.default_rng(9)
+    n, L, d = 6, 90, 16
+    q = rng.standard_normal((n, d))
+    k = rng.standard_normal((L, d))
+    v = rng.standard_normal((L, d))
+    prefix = L - n
+    lim = prefix + np.arange(n)
+    keys = np.arange(L)
+    full = ref.softmax_attention(q, k, v, 0.3, keys[None] <= lim[:, None])
+    for cuts in ([40], [16, 48, 80], [1, 2, 83]):
+        edges = [0] + cuts + [L]
+        parts = []
+        for a, c in zip(edges[:-1], edges[1:]):
+            vis = (keys[None] <= lim[:, None]) & (keys[None] >= a) & (keys[None] < c)
+            assert vis.any(axis=1).all()
+            parts.append(ref.softmax_attention(q, k, v, 0.3, vis))
+        o, l = ref.lse_merge(parts)
+        np.testing.assert_allclose(o, full[0], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(l, full[1], rtol=0, atol=1e-12)
+
+
+def test_row_independence():
+    specs = [SeqSpec(40, 1), SeqSpec(64, 16), SeqSpec(23, 1), SeqSpec(19, 3)]
+    b = make_batch(specs, HeadSpec(4, 2, 16, 16), "bf16", 10)
+    o, l = run_oracle(b)
+    for s in range(len(specs)):
+        t0, t1 = b.query_start_loc[s], b.query_start_loc[s + 1]
+        os_, ls = ref.attention_reference(
+            b.q[t0:t1], b.k_cache, b.v_cache, b.k_new[t0:t1], b.v_new[t0:t1], b.block_tables[s:s + 1],
+            b.seq_lens[s:s + 1], np.array([0, t1 - t0], np.int32), b.scale, 2, 16, "bf16")
+        assert np.array_equal(os_, o[t0:t1]) and np.array_equal(ls, l[t0:t1])
+
+
+# ----------------------------------------------------------------------------
+# append
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_append_reference(dtype):
+    specs = [SeqSpec(70, 1), SeqSpec(50, 13), SeqSpec(17, 0), SeqSpec(64, 64), SeqSpec(33, 2)]
+    hq, hkv, d, bs = 4, 2, 16, 16
+    b = make_batch(specs, HeadSpec(hq, hkv, d, bs), dtype, 11)
+    kc, vc = ref.append_reference(b.k_cache, b.v_cache, b.k_new, b.v_new, b.block_tables, b.seq_lens,
+                                  b.query_start_loc, bs, dtype)
+    x = 16 // (2 if dtype == "bf16" else 4)
+    touched_k = np.zeros(kc.size, bool)
+    touched_v = np.zeros(vc.size, bool)
+    kflat, vflat = kc.ravel(), vc.ravel()
+    for s, sp in enumerate(specs):
+        t0 = int(b.query_start_loc[s])
+        for i in range(sp.q_len):
+            p = sp.ctx - sp.q_len + i
+            blk = int(b.block_tables[s, p // bs])
+            for h in range(hkv):
+                for c in range(d):
+                    fk = _flat_k(blk, h, p % bs, c, hkv, d, bs, x)
+                    fv = _flat_v(blk, h, p % bs, c, hkv, d, bs)
+                    assert kflat[fk].tobytes() == b.k_new[t0 + i, h, c].tobytes()
+                    assert vflat[fv].tobytes() == b.v_new[t0 + i, h, c].tobytes()
+                    touched_k[fk] = touched_v[fv] = True
+    assert kc.ravel()[~touched_k].tobytes() == b.k_cache.ravel()[~touched_k].tobytes()
+    assert vc.ravel()[~touched_v].tobytes() == b.v_cache.ravel()[~touched_v].tobytes()
+    # Attending over the appended pool with no new tokens gives the same rows.
+    o1, l1 = run_oracle(b)
+    for s, sp in enumerate(specs):
+        if sp.q_len == 0:
+            continue
+        k, v = ref.gather_kv(kc, vc, b.block_tables[s], sp.ctx, hkv, d, bs, dtype)
+        t0 = int(b.query_start_loc[s])
+        o2, l2 = ref.sequence_attention(ref.decode_raw(b.q[t0:t0 + sp.q_len], dtype), k, v,
+                                        sp.ctx - sp.q_len, b.scale, hkv)
+        assert np.array_equal(o2, o1[t0:t0 + sp.q_len]) and np.array_equal(l2, l1[t0:t0 + sp.q_len])
+
+
+# ----------------------------------------------------------------------------
+# bf16 handling (decode in the oracle, round-to-nearest-even in the generator)
+
+
+def test_bf16_decode_and_rounding():
+    bits = np.array([0x3F80, 0xC000, 0x7F80, 0x0001, 0x8000], np.uint16)
+    got = ref.decode_raw(bits, "bf16")
+    assert list(got[:3]) == [1.0, -2.0, math.inf]
+    assert got[3] == 2.0 ** -133 and got[4] == 0.0 and math.copysign(1, got[4]) < 0
+    ties = np.array([1 + 2 ** -8, 1 + 3 * 2 ** -8, -(1 + 2 ** -8), np.nan], np.float32)
+    r = bf16_bits_from_f32(ties)
+    assert list(r[:3]) == [0x3F80, 0x3F82, 0xBF80] and r[3] == 0x7FC0
+    torch = pytest.importorskip("torch")
+    x = np.random.default_rng(12).standard_normal(100000, dtype=np.float32) * 100
+    tb = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(bf16_bits_from_f32(x), tb)
