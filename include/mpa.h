@@ -1,0 +1,186 @@
+/*
+ * mpa.h -- mixed prefill+decode paged attention for one MI355X (gfx950).
+ *
+ * One serving iteration of a decode node that lends compute to prefill work
+ * (Crossflow, arxiv 2609.27085): the decode node takes a whole request,
+ * reuses its resident prefix and runs the remaining prompt tokens as chunks
+ * inside the same batch as its running decode rows (section 4.4, "Spilled-
+ * request execution"; section 5, the local prefill queue and the mixed
+ * prefill/decode batch).  This library is that iteration's attention step:
+ * append the step's new K/V to a paged cache, then attend for every query
+ * row of the varlen batch through per-sequence block tables.
+ *
+ * ---------------------------------------------------------------------------
+ * Batch description (all int32):
+ *   S                  number of sequences in the step
+ *   query_start_loc    [S+1], query_start_loc[0] = 0, non-decreasing,
+ *                      query_start_loc[S] = T (total query tokens).  Sequence
+ *                      s owns query rows query_start_loc[s] .. [s+1]-1.
+ *   seq_lens           [S], KV length of sequence s AFTER this step's append.
+ *                      q_len(s) = query_start_loc[s+1] - query_start_loc[s]
+ *                      must satisfy 0 <= q_len(s) <= seq_lens[s].
+ *   block_tables       [S][max_blocks_per_seq], row-major; entry j of row s is
+ *                      the physical block holding logical positions
+ *                      16*j .. 16*j+15 of sequence s.  Only the first
+ *                      ceil(seq_lens[s] / 16) entries of a row are read.
+ *
+ * Positions and the causal rule: sequence s has a cached prefix of
+ * P = seq_lens[s] - q_len(s) tokens; its new token i (query row
+ * query_start_loc[s] + i) sits at logical position P + i and attends keys
+ * 0 .. P + i inclusive.  q_len = 1 is a decode row (it sees the whole
+ * context); q_len > 1 is a prefill chunk on the cached prefix; q_len = 0
+ * sequences are skipped.  Query head h reads KV head h / (Hq / Hkv).
+ *
+ * Tensors (device memory, dense, row-major; element type = shape.dtype):
+ *   q        [T][Hq][d]
+ *   k_new    [T][Hkv][d]      the step's new keys, row t = query row t
+ *   v_new    [T][Hkv][d]
+ *   out      [T][Hq][d]
+ *   lse      [T][Hq] float32, natural log of each row's softmax denominator
+ *   k_cache  [num_blocks][Hkv][d/X][16][X]   X = 16 / element bytes
+ *   v_cache  [num_blocks][Hkv][d][16]
+ * i.e. key element (block b, head h, slot t, dim i) is at
+ * k_cache[b][h][i/X][t][i%X] and value element (b, h, t, i) at
+ * v_cache[b][h][i][t].  A (block, head) is one contiguous 16*d-element
+ * granule of each cache.  Shared (prefix) blocks may appear in several
+ * rows; the slots a step appends to must be distinct.
+ *
+ * Supported: dtype bf16 or f32 (the caches, q, k_new, v_new and out all in
+ * that type), head_dim 64 or 128, block_size 16, Hq a multiple of Hkv with
+ * Hq / Hkv <= 16.
+ *
+ * Conventions:
+ *  - The caller owns every buffer.  The library allocates nothing and keeps
+ *    no state between calls; calls on different streams are independent.
+ *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
+ *    stream).  The host arrays are read before the call returns.
+ *  - Every check runs before the first launch: an error return means that
+ *    nothing was launched and no device memory was touched.  Devices ids in
+ *    block_tables that the host did not check (block_tables_host == NULL)
+ *    are also guarded on the device: a block id outside [0, num_blocks)
+ *    is never dereferenced; the rows that needed it come out as NaN, and
+ *    the append skips the token.
+ *  - Cache slots at positions >= seq_lens[s] and blocks no row references
+ *    never influence any output, whatever they hold (NaN and Inf included).
+ * ---------------------------------------------------------------------------
+ */
+#ifndef MPA_H_
+#define MPA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MPA_OK = 0,
+  MPA_ERR_INVALID = -1,     /* malformed arguments or batch metadata */
+  MPA_ERR_UNSUPPORTED = -2, /* a shape or dtype this build does not handle */
+  MPA_ERR_WORKSPACE = -3,   /* workspace missing or smaller than required */
+  MPA_ERR_HIP = -4          /* a HIP launch reported an error */
+} mpa_status;
+
+typedef enum { MPA_BF16 = 0, MPA_F32 = 1 } mpa_dtype;
+
+typedef struct {
+  int32_t num_seqs;           /* S */
+  int32_t num_q_heads;        /* Hq */
+  int32_t num_kv_heads;       /* Hkv */
+  int32_t head_dim;           /* d: 64 or 128 */
+  int32_t block_size;         /* must be 16 */
+  int32_t num_blocks;         /* physical blocks in each cache */
+  int32_t max_blocks_per_seq; /* row stride of block_tables */
+  int32_t total_q_tokens;     /* T = query_start_loc[S] */
+  float scale;                /* softmax scale, e.g. 1/sqrt(d) */
+  int32_t dtype;              /* mpa_dtype */
+} mpa_shape;
+
+/*
+ * Append the step's new keys and values to the paged cache.
+ *
+ * Defines: new token i of sequence s (query row query_start_loc[s] + i) is
+ * position p = seq_lens[s] - q_len(s) + i, and its Hkv*d key and value
+ * elements are copied, bit for bit, to slot p % 16 of block
+ * block_tables[s][p / 16] (paper, section 4.4: the chunk's KV is
+ * materialised on top of the reused prefix; section 2.1: decode extends the
+ * KV cache by one token per step).  No other cache element changes.
+ *
+ * k_new, v_new      device [T][Hkv][d]
+ * k_cache, v_cache  device caches (layout above), written in place
+ * block_tables, seq_lens, query_start_loc        device copies
+ * seq_lens_host, query_start_loc_host            host copies (must match)
+ * block_tables_host host copy [S][max_blocks_per_seq] or NULL; when given,
+ *                   every block id the step uses is checked on the host.
+ * Returns MPA_OK, or an error code with nothing launched.
+ */
+int mpa_kv_append(const mpa_shape* shape, const void* k_new, const void* v_new, void* k_cache,
+                  void* v_cache, const int32_t* block_tables, const int32_t* seq_lens,
+                  const int32_t* query_start_loc, const int32_t* seq_lens_host,
+                  const int32_t* query_start_loc_host, const int32_t* block_tables_host,
+                  void* stream);
+
+/*
+ * Bytes of device workspace that mpa_mixed_paged_attention needs for this
+ * batch (the split-K partial results of long decode rows).  Depends only on
+ * the shape and the host metadata.  Returns 0 for an invalid batch.
+ */
+size_t mpa_workspace_size(const mpa_shape* shape, const int32_t* seq_lens_host,
+                          const int32_t* query_start_loc_host);
+
+/*
+ * Attention for every query row of the mixed batch, reading K/V only from
+ * the (already appended) cache.
+ *
+ * Defines: for query row t of sequence s at position p and query head h,
+ *   out[t][h] = sum_{j<=p} softmax_j(scale * q[t][h] . k_j) v_j
+ * over sequence s's keys k_j, v_j (KV head h / (Hq/Hkv)), and
+ *   lse[t][h] = log sum_{j<=p} exp(scale * q[t][h] . k_j).
+ * The paper (section 2.1) has decode re-read the growing KV cache each
+ * step and (section 4.4, section 5) batches prefill chunks on cached
+ * prefixes with those decode rows; it does not write the formula out --
+ * this is standard scaled dot-product attention under the causal rule above.
+ *
+ * Decode rows (q_len = 1) run as split-K over KV blocks with an LSE merge;
+ * prefill chunks (q_len > 1) run as causal MFMA tiles.
+ *
+ * q                 device [T][Hq][d]
+ * out               device [T][Hq][d], written for every row of every
+ *                   sequence with q_len > 0
+ * lse               device [T][Hq] float32, or NULL
+ * workspace         device scratch of at least mpa_workspace_size() bytes
+ *                   (may be NULL when that is 0); contents on entry unused
+ * Other arguments as for mpa_kv_append.
+ */
+int mpa_mixed_paged_attention(const mpa_shape* shape, const void* q, const void* k_cache,
+                              const void* v_cache, const int32_t* block_tables,
+                              const int32_t* seq_lens, const int32_t* query_start_loc,
+                              const int32_t* seq_lens_host, const int32_t* query_start_loc_host,
+                              const int32_t* block_tables_host, void* out, float* lse,
+                              void* workspace, size_t workspace_bytes, void* stream);
+
+/* Static description of a status code. */
+const char* mpa_status_string(int status);
+
+/*
+ * Plan statistics for a batch (host only; launches nothing): how the
+ * library splits decode rows and tiles prefill chunks.
+ */
+typedef struct {
+  int32_t num_decode_seqs;   /* sequences with q_len == 1 */
+  int32_t num_prefill_seqs;  /* sequences with q_len > 1 */
+  int32_t split_tokens;      /* KV tokens per decode split */
+  int32_t num_decode_items;  /* (sequence, split) work items */
+  int32_t num_prefill_tiles; /* (sequence, query tile, KV head) work items */
+  int32_t decode_launches;   /* decode kernel launches (sequence chunks) */
+} mpa_plan_info;
+
+int mpa_get_plan_info(const mpa_shape* shape, const int32_t* seq_lens_host,
+                      const int32_t* query_start_loc_host, mpa_plan_info* info);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MPA_H_ */

@@ -1,0 +1,216 @@
+"""Python binding of ``libmpa.so`` (include/mpa.h): argument marshalling only.
+
+Every step of the attention path runs in the library's HIP kernels; this
+module turns torch device tensors into pointers, host numpy arrays into int32
+buffers and the current torch stream into a ``hipStream_t``.  If the library
+is not built the calls raise ``MpaUnavailable``; there is no fallback.
+
+    import paper_2609_27085_amd as mpa
+    mpa.kv_append(k_new, v_new, k_cache, v_cache, block_tables, seq_lens, qsl,
+                  seq_lens_host, qsl_host)
+    ws = mpa.alloc_workspace(q, k_cache, block_tables, seq_lens_host, qsl_host)
+    mpa.mixed_paged_attention(q, k_cache, v_cache, block_tables, seq_lens, qsl,
+                              seq_lens_host, qsl_host, out, lse=lse, workspace=ws)
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmpa.so")
+
+MPA_OK = 0
+MPA_ERR_INVALID = -1
+MPA_ERR_UNSUPPORTED = -2
+MPA_ERR_WORKSPACE = -3
+MPA_ERR_HIP = -4
+MPA_BF16 = 0
+MPA_F32 = 1
+BLOCK_SIZE = 16
+
+EXPORTS = (
+    "mpa_kv_append",
+    "mpa_mixed_paged_attention",
+    "mpa_workspace_size",
+    "mpa_status_string",
+    "mpa_get_plan_info",
+)
+
+
+class MpaUnavailable(RuntimeError):
+    pass
+
+
+class MpaError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {status_string(status)} ({status})")
+        self.status = status
+
+
+class MpaShape(ctypes.Structure):
+    _fields_ = [
+        ("num_seqs", ctypes.c_int32),
+        ("num_q_heads", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("block_size", ctypes.c_int32),
+        ("num_blocks", ctypes.c_int32),
+        ("max_blocks_per_seq", ctypes.c_int32),
+        ("total_q_tokens", ctypes.c_int32),
+        ("scale", ctypes.c_float),
+        ("dtype", ctypes.c_int32),
+    ]
+
+
+class MpaPlanInfo(ctypes.Structure):
+    _fields_ = [
+        ("num_decode_seqs", ctypes.c_int32),
+        ("num_prefill_seqs", ctypes.c_int32),
+        ("split_tokens", ctypes.c_int32),
+        ("num_decode_items", ctypes.c_int32),
+        ("num_prefill_tiles", ctypes.c_int32),
+        ("decode_launches", ctypes.c_int32),
+    ]
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I32P = ctypes.POINTER(ctypes.c_int32)
+_SHP = ctypes.POINTER(MpaShape)
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library (raises MpaUnavailable if it is not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise MpaUnavailable(f"{LIB_PATH} is missing; build it with `python -m paper_2609_27085_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        L.mpa_kv_append.restype = ctypes.c_int
+        L.mpa_kv_append.argtypes = [_SHP, _P, _P, _P, _P, _P, _P, _P, _I32P, _I32P, _I32P, _P]
+        L.mpa_mixed_paged_attention.restype = ctypes.c_int
+        L.mpa_mixed_paged_attention.argtypes = [
+            _SHP, _P, _P, _P, _P, _P, _P, _I32P, _I32P, _I32P, _P, _P, _P, ctypes.c_size_t, _P]
+        L.mpa_workspace_size.restype = ctypes.c_size_t
+        L.mpa_workspace_size.argtypes = [_SHP, _I32P, _I32P]
+        L.mpa_status_string.restype = ctypes.c_char_p
+        L.mpa_status_string.argtypes = [ctypes.c_int]
+        L.mpa_get_plan_info.restype = ctypes.c_int
+        L.mpa_get_plan_info.argtypes = [_SHP, _I32P, _I32P, ctypes.POINTER(MpaPlanInfo)]
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().mpa_status_string(int(status)).decode()
+
+
+def _host_i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a), dtype=np.int32)
+
+
+def _i32p(a: Optional[np.ndarray]):
+    if a is None:
+        return None
+    return a.ctypes.data_as(_I32P)
+
+
+def _dtype_code(t) -> int:
+    import torch
+
+    if t.dtype == torch.bfloat16:
+        return MPA_BF16
+    if t.dtype == torch.float32:
+        return MPA_F32
+    raise ValueError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def make_shape(num_seqs, num_q_heads, num_kv_heads, head_dim, num_blocks, max_blocks_per_seq, total_q_tokens,
+               scale, dtype: int, block_size: int = BLOCK_SIZE) -> MpaShape:
+    return MpaShape(int(num_seqs), int(num_q_heads), int(num_kv_heads), int(head_dim), int(block_size),
+                    int(num_blocks), int(max_blocks_per_seq), int(total_q_tokens), float(scale), int(dtype))
+
+
+def shape_of(q, k_cache, block_tables, seq_lens_host, scale=None) -> MpaShape:
+    """mpa_shape from the tensors: q [T, Hq, d], k_cache [NB, Hkv, d/X, 16, X]
+    (or any view with NB and Hkv leading), block_tables [S, MB]."""
+    t, hq, d = q.shape
+    if scale is None:
+        scale = 1.0 / float(d) ** 0.5
+    return make_shape(len(seq_lens_host), hq, k_cache.shape[1], d, k_cache.shape[0], block_tables.shape[1], t,
+                      scale, _dtype_code(q))
+
+
+def plan_info(shape: MpaShape, seq_lens_host, qsl_host) -> MpaPlanInfo:
+    sl, qs = _host_i32(seq_lens_host), _host_i32(qsl_host)
+    info = MpaPlanInfo()
+    rc = lib().mpa_get_plan_info(ctypes.byref(shape), _i32p(sl), _i32p(qs), ctypes.byref(info))
+    if rc != MPA_OK:
+        raise MpaError(rc, "mpa_get_plan_info")
+    return info
+
+
+def workspace_size(shape: MpaShape, seq_lens_host, qsl_host) -> int:
+    sl, qs = _host_i32(seq_lens_host), _host_i32(qsl_host)
+    return int(lib().mpa_workspace_size(ctypes.byref(shape), _i32p(sl), _i32p(qs)))
+
+
+def alloc_workspace(q, k_cache, block_tables, seq_lens_host, qsl_host, scale=None):
+    """A device byte tensor large enough for this batch (None if none needed)."""
+    import torch
+
+    n = workspace_size(shape_of(q, k_cache, block_tables, seq_lens_host, scale), seq_lens_host, qsl_host)
+    if n == 0:
+        return None
+    return torch.empty(n, dtype=torch.uint8, device=q.device)
+
+
+def kv_append(k_new, v_new, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host,
+              block_tables_host=None, stream=None) -> None:
+    """mpa_kv_append on torch device tensors (host metadata as arrays)."""
+    t, hkv, d = k_new.shape
+    sl, qs = _host_i32(seq_lens_host), _host_i32(qsl_host)
+    bth = None if block_tables_host is None else _host_i32(block_tables_host)
+    shape = make_shape(len(sl), hkv, hkv, d, k_cache.shape[0], block_tables.shape[1], t, 1.0, _dtype_code(k_new))
+    rc = lib().mpa_kv_append(
+        ctypes.byref(shape), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(block_tables),
+        _ptr(seq_lens), _ptr(query_start_loc), _i32p(sl), _i32p(qs), _i32p(bth), _stream(stream))
+    if rc != MPA_OK:
+        raise MpaError(rc, "mpa_kv_append")
+
+
+def mixed_paged_attention(q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host,
+                          out, lse=None, workspace=None, scale=None, block_tables_host=None, stream=None) -> None:
+    """mpa_mixed_paged_attention on torch device tensors."""
+    sl, qs = _host_i32(seq_lens_host), _host_i32(qsl_host)
+    bth = None if block_tables_host is None else _host_i32(block_tables_host)
+    shape = shape_of(q, k_cache, block_tables, sl, scale)
+    ws_ptr, ws_bytes = (None, 0) if workspace is None else (_ptr(workspace), workspace.numel() * workspace.element_size())
+    rc = lib().mpa_mixed_paged_attention(
+        ctypes.byref(shape), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_tables), _ptr(seq_lens),
+        _ptr(query_start_loc), _i32p(sl), _i32p(qs), _i32p(bth), _ptr(out), _ptr(lse), ws_ptr, ws_bytes,
+        _stream(stream))
+    if rc != MPA_OK:
+        raise MpaError(rc, "mpa_mixed_paged_attention")

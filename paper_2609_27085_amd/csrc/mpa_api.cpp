@@ -1,0 +1,266 @@
+// C ABI of the mixed paged-attention library: host-side validation, the
+// varlen planner (decode rows -> split-K work items, prefill chunks -> query
+// tiles) and the launch sequence.  Every check runs before the first launch.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "mpa.h"
+#include "mpa_internal.h"
+
+namespace {
+
+using mpa::kBlock;
+
+struct Batch {
+  std::vector<int> decode;   // sequence ids with q_len == 1
+  std::vector<int> prefill;  // sequence ids with q_len > 1
+  long decode_tokens = 0;    // sum of KV lengths of decode rows
+};
+
+int check_shape(const mpa_shape* sh) {
+  if (!sh) return MPA_ERR_INVALID;
+  if (sh->num_seqs < 0 || sh->num_q_heads <= 0 || sh->num_kv_heads <= 0 || sh->num_blocks < 0 ||
+      sh->max_blocks_per_seq < 0 || sh->total_q_tokens < 0 || !isfinite(sh->scale))
+    return MPA_ERR_INVALID;
+  if (sh->dtype != MPA_BF16 && sh->dtype != MPA_F32) return MPA_ERR_UNSUPPORTED;
+  if (sh->head_dim != 64 && sh->head_dim != 128) return MPA_ERR_UNSUPPORTED;
+  if (sh->block_size != kBlock) return MPA_ERR_UNSUPPORTED;
+  if (sh->num_q_heads % sh->num_kv_heads != 0) return MPA_ERR_UNSUPPORTED;
+  if (sh->num_q_heads / sh->num_kv_heads > 16) return MPA_ERR_UNSUPPORTED;
+  return MPA_OK;
+}
+
+// Validates the host metadata and classifies the sequences.
+int check_batch(const mpa_shape* sh, const int32_t* seq_lens, const int32_t* qsl, const int32_t* bt_host,
+                bool append_only, Batch* b) {
+  int rc = check_shape(sh);
+  if (rc != MPA_OK) return rc;
+  const int S = sh->num_seqs;
+  if (S > 0 && (!seq_lens || !qsl)) return MPA_ERR_INVALID;
+  if (S == 0) return sh->total_q_tokens == 0 ? MPA_OK : MPA_ERR_INVALID;
+  if (qsl[0] != 0 || qsl[S] != sh->total_q_tokens) return MPA_ERR_INVALID;
+  for (int s = 0; s < S; ++s) {
+    const int ql = qsl[s + 1] - qsl[s];
+    const int L = seq_lens[s];
+    if (ql < 0 || L < 0 || ql > L) return MPA_ERR_INVALID;
+    if (ql == 0) continue;
+    if (sh->num_blocks == 0) return MPA_ERR_INVALID;  // nothing could hold its KV
+    const long nblk = ((long)L + kBlock - 1) / kBlock;
+    if (nblk > sh->max_blocks_per_seq) return MPA_ERR_INVALID;
+    if (bt_host) {
+      const long first = append_only ? (long)(L - ql) / kBlock : 0;
+      for (long j = first; j < nblk; ++j) {
+        const int32_t id = bt_host[(size_t)s * sh->max_blocks_per_seq + j];
+        if (id < 0 || id >= sh->num_blocks) return MPA_ERR_INVALID;
+      }
+    }
+    if (ql == 1) {
+      b->decode.push_back(s);
+      b->decode_tokens += L;
+    } else {
+      b->prefill.push_back(s);
+    }
+  }
+  return MPA_OK;
+}
+
+// KV tokens per decode split: enough (item, KV head) waves to fill the chip
+// several times over, in powers of two from 256 to 8192 tokens.  Overridable
+// with MPA_SPLIT_TOKENS (a multiple of 16) for tuning sweeps.
+int choose_split(const mpa_shape* sh, const Batch& b) {
+  if (const char* env = getenv("MPA_SPLIT_TOKENS")) {
+    const int v = atoi(env);
+    if (v >= kBlock && v % kBlock == 0) return v;
+  }
+  const long target_waves = 256L * 32;  // 256 CUs, 32 waves each
+  int split = 256;
+  while (split < 8192 && (b.decode_tokens / split + (long)b.decode.size()) * sh->num_kv_heads > target_waves)
+    split *= 2;
+  return split;
+}
+
+long decode_items(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens, int split) {
+  (void)sh;
+  long n = 0;
+  for (int s : b.decode) n += std::max(1, (seq_lens[s] + split - 1) / split);
+  return n;
+}
+
+int q_tile(const mpa_shape* sh) { return mpa::kPrefillRows / (sh->num_q_heads / sh->num_kv_heads); }
+
+size_t workspace_bytes(const mpa_shape* sh, long items) {
+  const size_t per = (size_t)sh->num_q_heads * (sh->head_dim + 2) * sizeof(float);
+  return items * per;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mpa_status_string(int status) {
+  switch (status) {
+    case MPA_OK: return "ok";
+    case MPA_ERR_INVALID: return "invalid argument or batch metadata";
+    case MPA_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+    case MPA_ERR_WORKSPACE: return "workspace missing or too small";
+    case MPA_ERR_HIP: return "HIP launch error";
+    default: return "unknown status";
+  }
+}
+
+int mpa_get_plan_info(const mpa_shape* shape, const int32_t* seq_lens_host, const int32_t* qsl_host,
+                      mpa_plan_info* info) {
+  if (!info) return MPA_ERR_INVALID;
+  Batch b;
+  int rc = check_batch(shape, seq_lens_host, qsl_host, nullptr, false, &b);
+  if (rc != MPA_OK) return rc;
+  const int split = choose_split(shape, b);
+  info->num_decode_seqs = (int32_t)b.decode.size();
+  info->num_prefill_seqs = (int32_t)b.prefill.size();
+  info->split_tokens = split;
+  info->num_decode_items = (int32_t)decode_items(shape, b, seq_lens_host, split);
+  long tiles = 0;
+  const int qt = q_tile(shape);
+  for (int s : b.prefill) tiles += (qsl_host[s + 1] - qsl_host[s] + qt - 1) / qt;
+  info->num_prefill_tiles = (int32_t)(tiles * shape->num_kv_heads);
+  info->decode_launches = (int32_t)((b.decode.size() + mpa::kMaxPlanSeqs - 1) / mpa::kMaxPlanSeqs);
+  return MPA_OK;
+}
+
+size_t mpa_workspace_size(const mpa_shape* shape, const int32_t* seq_lens_host, const int32_t* qsl_host) {
+  Batch b;
+  if (check_batch(shape, seq_lens_host, qsl_host, nullptr, false, &b) != MPA_OK) return 0;
+  const int split = choose_split(shape, b);
+  bool any_split = false;
+  for (int s : b.decode) any_split |= seq_lens_host[s] > split;
+  if (!any_split) return 0;
+  return workspace_bytes(shape, decode_items(shape, b, seq_lens_host, split));
+}
+
+int mpa_kv_append(const mpa_shape* shape, const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                  const int32_t* block_tables, const int32_t* seq_lens, const int32_t* query_start_loc,
+                  const int32_t* seq_lens_host, const int32_t* query_start_loc_host,
+                  const int32_t* block_tables_host, void* stream) {
+  Batch b;
+  int rc = check_batch(shape, seq_lens_host, query_start_loc_host, block_tables_host, true, &b);
+  if (rc != MPA_OK) return rc;
+  if (shape->total_q_tokens == 0) return MPA_OK;
+  if (!k_new || !v_new || !k_cache || !v_cache || !block_tables || !seq_lens || !query_start_loc)
+    return MPA_ERR_INVALID;
+  mpa::AppendArgs a;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.block_tables = block_tables;
+  a.seq_lens = seq_lens;
+  a.qsl = query_start_loc;
+  a.num_seqs = shape->num_seqs;
+  a.total_q = shape->total_q_tokens;
+  a.hkv = shape->num_kv_heads;
+  a.mb = shape->max_blocks_per_seq;
+  a.nb = shape->num_blocks;
+  hipError_t e = mpa::launch_append(a, shape->dtype, shape->head_dim, (hipStream_t)stream);
+  return e == hipSuccess ? MPA_OK : MPA_ERR_HIP;
+}
+
+int mpa_mixed_paged_attention(const mpa_shape* shape, const void* q, const void* k_cache, const void* v_cache,
+                              const int32_t* block_tables, const int32_t* seq_lens, const int32_t* query_start_loc,
+                              const int32_t* seq_lens_host, const int32_t* query_start_loc_host,
+                              const int32_t* block_tables_host, void* out, float* lse, void* workspace,
+                              size_t workspace_bytes_given, void* stream) {
+  Batch b;
+  int rc = check_batch(shape, seq_lens_host, query_start_loc_host, block_tables_host, false, &b);
+  if (rc != MPA_OK) return rc;
+  if (b.decode.empty() && b.prefill.empty()) return MPA_OK;
+  if (!q || !k_cache || !v_cache || !block_tables || !seq_lens || !query_start_loc || !out)
+    return MPA_ERR_INVALID;
+  const int split = choose_split(shape, b);
+  const long items = decode_items(shape, b, seq_lens_host, split);
+  bool any_split = false;
+  for (int s : b.decode) any_split |= seq_lens_host[s] > split;
+  if (any_split) {
+    const size_t need = workspace_bytes(shape, items);
+    if (!workspace || workspace_bytes_given < need) return MPA_ERR_WORKSPACE;
+  }
+
+  mpa::AttnArgs a;
+  a.q = q;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.block_tables = block_tables;
+  a.seq_lens = seq_lens;
+  a.qsl = query_start_loc;
+  a.out = out;
+  a.lse = lse;
+  a.ws_o = any_split ? static_cast<float*>(workspace) : nullptr;
+  a.ws_ml = any_split ? a.ws_o + (size_t)items * shape->num_q_heads * shape->head_dim : nullptr;
+  a.hq = shape->num_q_heads;
+  a.hkv = shape->num_kv_heads;
+  a.mb = shape->max_blocks_per_seq;
+  a.nb = shape->num_blocks;
+  a.scale_log2 = shape->scale * 1.4426950408889634f;
+  hipStream_t st = (hipStream_t)stream;
+
+  // Decode rows, in launches of up to kMaxPlanSeqs sequences.
+  std::vector<mpa::DecodePlan> dplans;
+  {
+    long base = 0;
+    for (size_t c0 = 0; c0 < b.decode.size(); c0 += mpa::kMaxPlanSeqs) {
+      mpa::DecodePlan p;
+      memset(&p, 0, sizeof(p));
+      const size_t c1 = std::min(b.decode.size(), c0 + mpa::kMaxPlanSeqs);
+      p.n_seqs = (int32_t)(c1 - c0);
+      p.split_tokens = split;
+      p.item_base = (int32_t)base;
+      int acc = 0;
+      for (size_t k = c0; k < c1; ++k) {
+        const int s = b.decode[k];
+        p.seq[k - c0] = s;
+        p.item_start[k - c0] = acc;
+        acc += std::max(1, (seq_lens_host[s] + split - 1) / split);
+      }
+      p.item_start[c1 - c0] = acc;
+      base += acc;
+      dplans.push_back(p);
+    }
+  }
+  for (const auto& p : dplans) {
+    hipError_t e = mpa::launch_decode(a, p, p.item_start[p.n_seqs], shape->dtype, shape->head_dim, st);
+    if (e != hipSuccess) return MPA_ERR_HIP;
+  }
+  if (any_split) {
+    for (const auto& p : dplans) {
+      hipError_t e = mpa::launch_merge(a, p, shape->dtype, shape->head_dim, st);
+      if (e != hipSuccess) return MPA_ERR_HIP;
+    }
+  }
+  // Prefill chunks.
+  const int qt = q_tile(shape);
+  for (size_t c0 = 0; c0 < b.prefill.size(); c0 += mpa::kMaxPlanSeqs) {
+    mpa::PrefillPlan p;
+    memset(&p, 0, sizeof(p));
+    const size_t c1 = std::min(b.prefill.size(), c0 + mpa::kMaxPlanSeqs);
+    p.n_seqs = (int32_t)(c1 - c0);
+    p.q_tile = qt;
+    int acc = 0;
+    for (size_t k = c0; k < c1; ++k) {
+      const int s = b.prefill[k];
+      p.seq[k - c0] = s;
+      p.tile_start[k - c0] = acc;
+      acc += (query_start_loc_host[s + 1] - query_start_loc_host[s] + qt - 1) / qt;
+    }
+    p.tile_start[c1 - c0] = acc;
+    hipError_t e = mpa::launch_prefill(a, p, acc, shape->dtype, shape->head_dim, st);
+    if (e != hipSuccess) return MPA_ERR_HIP;
+  }
+  return MPA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,73 @@
+// Internal plan structures shared by the host planner (mpa_api.cpp) and the
+// kernels (mpa_kernels.hip).  Plans travel as kernel arguments, so a launch
+// needs no host-to-device copy and no device allocation.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mpa {
+
+constexpr int kBlock = 16;            // tokens per cache block
+constexpr int kWavesPerGroup = 4;     // waves per workgroup in every kernel
+constexpr int kMaxPlanSeqs = 256;     // sequences per launch (kernel-argument plan)
+constexpr int kPrefillRows = 64;      // (token, head) rows per prefill workgroup
+
+// Pointers and sizes common to the attention kernels.
+struct AttnArgs {
+  const void* q;
+  const void* k_cache;
+  const void* v_cache;
+  const int32_t* block_tables;
+  const int32_t* seq_lens;
+  const int32_t* qsl;
+  void* out;
+  float* lse;        // may be null
+  float* ws_o;       // [items][Hq][d] split partial accumulators
+  float* ws_ml;      // [items][Hq][2] split partial (max, sum); max in log2 units
+  int32_t hq, hkv, mb, nb;
+  float scale_log2;  // softmax scale * log2(e)
+};
+
+// Decode work for up to kMaxPlanSeqs sequences: item k of this launch is
+// split (k - item_start[j]) of sequence seq[j], where item_start[j] <= k <
+// item_start[j+1].  Its partial results live at workspace slot
+// item_base + k.
+struct DecodePlan {
+  int32_t n_seqs;
+  int32_t split_tokens;
+  int32_t item_base;
+  int32_t seq[kMaxPlanSeqs];
+  int32_t item_start[kMaxPlanSeqs + 1];
+};
+
+// Prefill work for up to kMaxPlanSeqs sequences: query tile k of this launch
+// is tile (k - tile_start[j]) of sequence seq[j]; grid.y is the KV head.
+struct PrefillPlan {
+  int32_t n_seqs;
+  int32_t q_tile;    // query tokens per tile = kPrefillRows / G
+  int32_t seq[kMaxPlanSeqs];
+  int32_t tile_start[kMaxPlanSeqs + 1];
+};
+
+struct AppendArgs {
+  const void* k_new;
+  const void* v_new;
+  void* k_cache;
+  void* v_cache;
+  const int32_t* block_tables;
+  const int32_t* seq_lens;
+  const int32_t* qsl;
+  int32_t num_seqs, total_q, hkv, mb, nb;
+};
+
+// Launchers (mpa_kernels.hip).  dtype: 0 = bf16, 1 = f32.  Return the HIP
+// error of the launch.
+hipError_t launch_append(const AppendArgs& a, int dtype, int head_dim, hipStream_t stream);
+hipError_t launch_decode(const AttnArgs& a, const DecodePlan& p, int n_items, int dtype, int head_dim,
+                         hipStream_t stream);
+hipError_t launch_merge(const AttnArgs& a, const DecodePlan& p, int dtype, int head_dim, hipStream_t stream);
+hipError_t launch_prefill(const AttnArgs& a, const PrefillPlan& p, int n_tiles, int dtype, int head_dim,
+                          hipStream_t stream);
+
+}  // namespace mpa

@@ -1,0 +1,321 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Every case draws seeded inputs, runs mpa_kv_append then
+mpa_mixed_paged_attention on the GPU, and compares with the oracle run on the
+same arrays: the append bit for bit over the whole pool, attention outputs to
+max |err| <= 1e-2 and mean |err| <= 1e-3 for bf16 (1e-4 / 1e-5 for f32), and
+the log-sum-exp to 1e-4.
+"""
+
+import dataclasses
+import sys
+
+import numpy as np
+import pytest
+
+import paper_2609_27085_amd as mpa
+from oracle import ref
+from workloads import HeadSpec, SeqSpec, make_batch
+from workloads.configs import config_batch, config_specs
+from workloads.device import device_step, host_subbatch, tensor_to_raw, to_device
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"bf16": (1e-2, 1e-3), "f32": (1e-4, 1e-5)}
+LSE_TOL = 1e-4
+
+
+@pytest.fixture(scope="module")
+def torch_gpu():
+    import torch
+
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    mpa.lib()  # fail loudly if the library is not built
+    return torch
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def run_step(d, lse=True, append=True):
+    """append + attention on the GPU; returns (out, lse) device tensors."""
+    import torch
+
+    if append:
+        mpa.kv_append(d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
+                      d.seq_lens_host, d.qsl_host, block_tables_host=d.block_tables_host)
+    out = torch.full_like(d.q, float("nan"))
+    l = torch.full(d.q.shape[:2], float("nan"), dtype=torch.float32, device=d.q.device) if lse else None
+    ws = mpa.alloc_workspace(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.qsl_host, d.scale)
+    mpa.mixed_paged_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
+                              d.seq_lens_host, d.qsl_host, out, lse=l, workspace=ws, scale=d.scale,
+                              block_tables_host=d.block_tables_host)
+    torch.cuda.synchronize()
+    return out, l
+
+
+def as_f64(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def oracle_for(b):
+    return ref.attention_reference(b.q, b.k_cache, b.v_cache, b.k_new, b.v_new, b.block_tables, b.seq_lens,
+                                   b.query_start_loc, b.scale, b.heads.num_kv_heads, b.heads.block_size, b.dtype)
+
+
+def assert_close(got, exp, dtype, what=""):
+    mx, mean = TOL[dtype]
+    assert np.isfinite(got).all(), f"{what}: non-finite output"
+    err = np.abs(got - exp)
+    assert err.max() <= mx, f"{what}: max err {err.max():.3g} > {mx}"
+    assert err.mean() <= mean, f"{what}: mean err {err.mean():.3g} > {mean}"
+
+
+def check_batch(b, what):
+    """Full parity of one host batch (append bit-exact + attention)."""
+    say(f"[gpu] {what}: S={b.num_seqs} T={b.total_q} heads={b.heads} dtype={b.dtype}")
+    d = to_device(b)
+    out, lse = run_step(d)
+    kc, vc = ref.append_reference(b.k_cache, b.v_cache, b.k_new, b.v_new, b.block_tables, b.seq_lens,
+                                  b.query_start_loc, b.heads.block_size, b.dtype)
+    assert tensor_to_raw(d.k_cache, b.dtype).tobytes() == kc.tobytes(), f"{what}: K append not bit-exact"
+    assert tensor_to_raw(d.v_cache, b.dtype).tobytes() == vc.tobytes(), f"{what}: V append not bit-exact"
+    o_ref, l_ref = oracle_for(b)
+    rows = np.repeat(b.q_lens > 0, b.q_lens)
+    assert_close(as_f64(out)[rows], o_ref[rows], b.dtype, what)
+    lg = lse.cpu().numpy().astype(np.float64)[rows]
+    assert np.abs(lg - l_ref[rows]).max() <= LSE_TOL, f"{what}: lse err {np.abs(lg - l_ref[rows]).max():.3g}"
+    return d, out, lse
+
+
+# ----------------------------------------------------------------------------
+# small configurations, whole-batch parity
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("seed", [0, 1, 2, 3, 4])
+def test_tiny_config(torch_gpu, dtype, seed):
+    check_batch(config_batch("tiny", seed, dtype), f"tiny seed={seed}")
+
+
+MIXES = [
+    # (Hq, Hkv, d)
+    (8, 8, 128),
+    (8, 4, 64),
+    (32, 8, 128),
+    (64, 8, 128),
+    (16, 1, 64),
+    (12, 4, 128),
+]
+
+
+def mixed_specs(rng):
+    specs = [SeqSpec(int(c), 1) for c in rng.integers(1, 2600, size=9)]
+    specs += [SeqSpec(1, 1), SeqSpec(16, 1), SeqSpec(17, 1), SeqSpec(5000, 1)]
+    specs += [SeqSpec(37, 37), SeqSpec(250 + 100, 100), SeqSpec(32, 16), SeqSpec(2, 2), SeqSpec(40, 0),
+              SeqSpec(300 + 129, 129), SeqSpec(16, 0)]
+    order = rng.permutation(len(specs))
+    return [specs[i] for i in order]
+
+
+@pytest.mark.parametrize("heads", MIXES, ids=lambda h: f"hq{h[0]}_hkv{h[1]}_d{h[2]}")
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_mixed_batches(torch_gpu, heads, dtype):
+    rng = np.random.default_rng(hash(heads) % 1000)
+    specs = mixed_specs(rng)
+    b = make_batch(specs, HeadSpec(*heads, 16), dtype, rng)
+    check_batch(b, f"mixed {heads}")
+
+
+def test_decode_only_and_prefill_only(torch_gpu):
+    rng = np.random.default_rng(21)
+    dec = [SeqSpec(int(c), 1) for c in rng.integers(1, 4000, size=20)]
+    check_batch(make_batch(dec, HeadSpec(32, 8, 128), "bf16", rng), "decode only")
+    pre = [SeqSpec(300, 300), SeqSpec(1000, 64), SeqSpec(70, 65)]
+    check_batch(make_batch(pre, HeadSpec(32, 8, 128), "bf16", rng), "prefill only")
+
+
+def test_many_sequences_span_several_launches(torch_gpu):
+    # more than 256 decode rows and 256 prefill chunks: several plan launches
+    rng = np.random.default_rng(22)
+    specs = [SeqSpec(int(c), 1) for c in rng.integers(1, 700, size=300)]
+    specs += [SeqSpec(int(p) + 3, 3) for p in rng.integers(0, 40, size=260)]
+    b = make_batch(specs, HeadSpec(8, 2, 64), "bf16", rng)
+    check_batch(b, "600 sequences")
+
+
+# ----------------------------------------------------------------------------
+# properties
+
+
+def test_context_one_returns_v_exactly(torch_gpu):
+    for dtype in ("bf16", "f32"):
+        b = make_batch([SeqSpec(1, 1)] * 5, HeadSpec(16, 4, 128), dtype, 23)
+        d = to_device(b)
+        out, _ = run_step(d)
+        v = tensor_to_raw(d.v_new, dtype)
+        got = tensor_to_raw(out, dtype)
+        for h in range(16):
+            assert got[:, h].tobytes() == v[:, h // 4].tobytes()
+
+
+def test_block_permutation_bit_identical(torch_gpu):
+    import torch
+
+    rng = np.random.default_rng(24)
+    b = make_batch(mixed_specs(rng), HeadSpec(32, 8, 128), "bf16", rng)
+    d1 = to_device(b)
+    o1, l1 = run_step(d1)
+    perm = rng.permutation(b.num_blocks)
+    inv = np.argsort(perm)
+    b2 = dataclasses.replace(
+        b, k_cache=b.k_cache[inv].copy(), v_cache=b.v_cache[inv].copy(),
+        block_tables=np.where(b.block_tables >= 0, perm[np.maximum(b.block_tables, 0)], -1).astype(np.int32))
+    d2 = to_device(b2)
+    o2, l2 = run_step(d2)
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(l1, l2)
+
+
+def test_mixed_equals_parts(torch_gpu):
+    import torch
+
+    rng = np.random.default_rng(25)
+    specs = mixed_specs(rng)
+    b = make_batch(specs, HeadSpec(32, 8, 128), "bf16", rng)
+    o_all, l_all = run_step(to_device(b))
+    q_lens = b.q_lens
+    for part in (q_lens == 1, q_lens > 1):
+        # same sequences; those outside the part get q_len 0
+        ql = np.where(part, q_lens, 0)
+        keep_rows = np.repeat(part, q_lens)
+        sub = dataclasses.replace(
+            b, query_start_loc=np.concatenate([[0], np.cumsum(ql)]).astype(np.int32),
+            q=b.q[keep_rows], k_new=b.k_new[keep_rows], v_new=b.v_new[keep_rows])
+        o, l = run_step(to_device(sub))
+        rows = torch.from_numpy(np.nonzero(keep_rows)[0]).cuda()
+        assert torch.equal(o.view(torch.int16), o_all.index_select(0, rows).view(torch.int16))
+        assert torch.equal(l, l_all.index_select(0, rows))
+
+
+def test_run_to_run_deterministic(torch_gpu):
+    import torch
+
+    rng = np.random.default_rng(26)
+    b = make_batch(mixed_specs(rng), HeadSpec(64, 8, 128), "bf16", rng)
+    d = to_device(b)
+    o1, l1 = run_step(d)
+    o2, l2 = run_step(d, append=False)
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)) and torch.equal(l1, l2)
+
+
+def test_inf_in_unread_slots_never_leaks(torch_gpu):
+    rng = np.random.default_rng(27)
+    b = make_batch(mixed_specs(rng), HeadSpec(32, 8, 128), "bf16", rng)
+    for arr in (b.k_cache, b.v_cache):
+        nan = arr == 0x7FC0
+        arr[nan] = np.where(rng.random(nan.sum()) < 0.5, 0x7F80, 0xFF80).astype(np.uint16)
+    check_batch(b, "inf sentinels")
+
+
+def test_workspace_too_small_launches_nothing(torch_gpu):
+    import torch
+
+    b = make_batch([SeqSpec(3000, 1), SeqSpec(50, 10)], HeadSpec(8, 2, 128), "bf16", 28)
+    d = to_device(b)
+    out = torch.zeros_like(d.q)
+    need = mpa.workspace_size(mpa.shape_of(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.scale),
+                              d.seq_lens_host, d.qsl_host)
+    assert need > 0
+    ws = torch.empty(need - 4, dtype=torch.uint8, device="cuda")
+    with pytest.raises(mpa.MpaError) as e:
+        mpa.mixed_paged_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
+                                  d.seq_lens_host, d.qsl_host, out, workspace=ws, scale=d.scale)
+    assert e.value.status == mpa.MPA_ERR_WORKSPACE
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(out) == 0
+
+
+def test_bad_device_block_id_gives_nan_not_fault(torch_gpu):
+    """A block id outside the pool that the host did not check is never
+    dereferenced: the rows that need it come out NaN, the others are right."""
+    import torch
+
+    b = make_batch([SeqSpec(100, 1), SeqSpec(60, 1), SeqSpec(40, 20)], HeadSpec(8, 2, 64), "bf16", 29)
+    o_ref, _ = oracle_for(b)
+    d = to_device(b)
+    mpa.kv_append(d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
+                  d.seq_lens_host, d.qsl_host)
+    bt = d.block_tables.clone()
+    bt[0, 2] = b.num_blocks + 1000  # sequence 0 reads it; no host table is passed
+    out = torch.zeros_like(d.q)
+    mpa.mixed_paged_attention(d.q, d.k_cache, d.v_cache, bt, d.seq_lens, d.query_start_loc, d.seq_lens_host,
+                              d.qsl_host, out, scale=d.scale)
+    torch.cuda.synchronize()
+    got = as_f64(out)
+    assert np.isnan(got[0]).all()
+    assert_close(got[1:], o_ref[1:], "bf16", "rows that do not read the bad block")
+
+
+# ----------------------------------------------------------------------------
+# full sizes, sampled rows
+
+
+def oracle_rows(b, s, rows):
+    """Oracle outputs of chosen rows (indices within the sequence) of sequence
+    s of a host batch, computed row by row."""
+    hq, hkv, d = b.heads.num_q_heads, b.heads.num_kv_heads, b.heads.head_dim
+    t0 = int(b.query_start_loc[s])
+    c = int(b.query_start_loc[s + 1]) - t0
+    L = int(b.seq_lens[s])
+    P = L - c
+    kp, vp = ref.gather_kv(b.k_cache, b.v_cache, b.block_tables[s], P, hkv, d, b.heads.block_size, b.dtype)
+    k = np.concatenate([kp, ref.decode_raw(b.k_new[t0:t0 + c], b.dtype)])
+    v = np.concatenate([vp, ref.decode_raw(b.v_new[t0:t0 + c], b.dtype)])
+    q = ref.decode_raw(b.q[t0:t0 + c], b.dtype)
+    rows = np.asarray(rows)
+    vis = np.arange(L)[None, :] <= (P + rows)[:, None]
+    kh = [np.ascontiguousarray(k[:, g]) for g in range(hkv)]
+    vh = [np.ascontiguousarray(v[:, g]) for g in range(hkv)]
+    out = np.empty((len(rows), hq, d))
+    lse = np.empty((len(rows), hq))
+    for h in range(hq):
+        g = h // (hq // hkv)
+        out[:, h], lse[:, h] = ref.softmax_attention(q[rows, h], kh[g], vh[g], b.scale, vis)
+    return out, lse
+
+
+FULL = ["decode8b", "lent", "agentic", "budget0", "budget256", "budget1024", "budget4096", "longctx"]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_size_sampled(torch_gpu, name):
+    import torch
+
+    seed = 0
+    specs, heads, nb, rng = config_specs(name, seed)
+    say(f"[gpu] full size {name}: {len(specs)} seqs, T={sum(s.q_len for s in specs)}")
+    d = device_step(specs, heads, "bf16", rng, seed, num_blocks=nb)
+    srng = np.random.default_rng(1000 + seed)
+    dec = [i for i, s in enumerate(specs) if s.q_len == 1]
+    pre = [i for i, s in enumerate(specs) if s.q_len > 1]
+    longest = max(dec, key=lambda i: specs[i].ctx) if dec else None
+    pick = sorted(set(([longest] if longest is not None else []) + list(srng.choice(dec, size=min(3, len(dec)),
+                                                                                    replace=False)) + pre))
+    sub = host_subbatch(d, pick)  # pre-append contents
+    b = sub["batch"]
+    out, lse = run_step(d)
+    got = as_f64(out)
+    lg = lse.cpu().numpy().astype(np.float64)
+    assert np.isfinite(got).all()
+    for k, s in enumerate(pick):
+        c = int(b.query_start_loc[k + 1] - b.query_start_loc[k])
+        rows = sorted(set([0, c - 1] + list(srng.integers(0, c, size=min(c, 6)))))
+        o_ref, l_ref = oracle_rows(b, k, rows)
+        g_rows = int(d.qsl_host[s]) + np.asarray(rows)
+        assert_close(got[g_rows], o_ref, "bf16", f"{name} seq {s} rows {rows}")
+        assert np.abs(lg[g_rows] - l_ref).max() <= LSE_TOL
+    del d
+    torch.cuda.empty_cache()

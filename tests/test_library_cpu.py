@@ -1,0 +1,150 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every function include/mpa.h declares, and rejects malformed batches before
+touching the device (nothing here launches a kernel)."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2609_27085_amd as mpa
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mpa.h")
+FAKE = 0x1000  # a non-null pointer value; never dereferenced because validation fails first
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(mpa_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = mpa.lib()
+    names = declared_functions()
+    assert set(names) == set(mpa.EXPORTS)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings():
+    for code in (0, -1, -2, -3, -4):
+        assert mpa.status_string(code)
+    assert mpa.status_string(123) == "unknown status"
+
+
+def shape(**kw):
+    base = dict(num_seqs=2, num_q_heads=8, num_kv_heads=2, head_dim=128, num_blocks=64, max_blocks_per_seq=8,
+                total_q_tokens=5, scale=0.1, dtype=mpa.MPA_BF16)
+    base.update(kw)
+    return mpa.make_shape(**base)
+
+
+def attention_rc(sh, seq_lens, qsl, bt=None, ws=0):
+    L = mpa.lib()
+    sl = np.asarray(seq_lens, np.int32)
+    qs = np.asarray(qsl, np.int32)
+    bth = None if bt is None else np.asarray(bt, np.int32)
+    return L.mpa_mixed_paged_attention(
+        ctypes.byref(sh), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, mpa._i32p(sl), mpa._i32p(qs), mpa._i32p(bth), FAKE,
+        None, None, ws, None)
+
+
+def append_rc(sh, seq_lens, qsl, bt=None):
+    L = mpa.lib()
+    sl = np.asarray(seq_lens, np.int32)
+    qs = np.asarray(qsl, np.int32)
+    bth = None if bt is None else np.asarray(bt, np.int32)
+    return L.mpa_kv_append(ctypes.byref(sh), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, mpa._i32p(sl), mpa._i32p(qs),
+                           mpa._i32p(bth), None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(head_dim=96), mpa.MPA_ERR_UNSUPPORTED),
+    (dict(head_dim=256), mpa.MPA_ERR_UNSUPPORTED),
+    (dict(block_size=32), mpa.MPA_ERR_UNSUPPORTED),
+    (dict(num_q_heads=6, num_kv_heads=4), mpa.MPA_ERR_UNSUPPORTED),
+    (dict(num_q_heads=64, num_kv_heads=2), mpa.MPA_ERR_UNSUPPORTED),
+    (dict(dtype=7), mpa.MPA_ERR_UNSUPPORTED),
+    (dict(num_kv_heads=0), mpa.MPA_ERR_INVALID),
+    (dict(scale=float("nan")), mpa.MPA_ERR_INVALID),
+])
+def test_unsupported_shapes_rejected(kw, code):
+    sh = shape(**kw)
+    assert attention_rc(sh, [40, 3], [0, 1, 5]) == code
+    assert append_rc(sh, [40, 3], [0, 1, 5]) == code
+
+
+@pytest.mark.parametrize("seq_lens,qsl", [
+    ([40, 3], [1, 1, 5]),      # query_start_loc[0] != 0
+    ([40, 3], [0, 1, 6]),      # query_start_loc[S] != T
+    ([40, 2], [0, 2, 5]),      # q_len 3 > seq_len 2
+    ([40, 3], [0, 6, 5]),      # negative q_len
+    ([-1, 3], [0, 0, 5]),      # negative seq_len
+    ([200, 3], [0, 1, 5]),     # 13 blocks > max_blocks_per_seq = 8
+])
+def test_bad_metadata_rejected(seq_lens, qsl):
+    sh = shape()
+    assert attention_rc(sh, seq_lens, qsl) == mpa.MPA_ERR_INVALID
+    assert append_rc(sh, seq_lens, qsl) == mpa.MPA_ERR_INVALID
+    assert mpa.lib().mpa_workspace_size(ctypes.byref(sh), mpa._i32p(np.asarray(seq_lens, np.int32)),
+                                        mpa._i32p(np.asarray(qsl, np.int32))) == 0
+
+
+def test_block_ids_checked_when_host_table_given():
+    sh = shape(num_blocks=10)
+    bt = np.zeros((2, 8), np.int32)
+    bt[0, :3] = [1, 2, 3]
+    bt[1, 0] = 4
+    bad = bt.copy()
+    bad[0, 2] = 10  # out of range, used by sequence 0 (40 tokens -> 3 blocks)
+    assert attention_rc(sh, [40, 3], [0, 1, 5], bad) == mpa.MPA_ERR_INVALID
+    assert append_rc(sh, [40, 3], [0, 1, 5], bad) == mpa.MPA_ERR_INVALID
+    neg = bt.copy()
+    neg[1, 0] = -1
+    assert attention_rc(sh, [40, 3], [0, 1, 5], neg) == mpa.MPA_ERR_INVALID
+
+
+def test_null_pointers_rejected():
+    L = mpa.lib()
+    sh = shape()
+    sl = np.asarray([40, 3], np.int32)
+    qs = np.asarray([0, 1, 5], np.int32)
+    assert L.mpa_mixed_paged_attention(ctypes.byref(sh), None, FAKE, FAKE, FAKE, FAKE, FAKE, mpa._i32p(sl),
+                                       mpa._i32p(qs), None, FAKE, None, None, 0, None) == mpa.MPA_ERR_INVALID
+    assert L.mpa_mixed_paged_attention(ctypes.byref(sh), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, mpa._i32p(qs),
+                                       None, FAKE, None, None, 0, None) == mpa.MPA_ERR_INVALID
+    assert L.mpa_mixed_paged_attention(None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, mpa._i32p(sl), mpa._i32p(qs),
+                                       None, FAKE, None, None, 0, None) == mpa.MPA_ERR_INVALID
+
+
+def test_workspace_required_for_split_rows():
+    sh = shape(max_blocks_per_seq=1024)
+    seq_lens, qsl = [9000, 40], [0, 1, 5]
+    n = mpa.workspace_size(sh, seq_lens, qsl)
+    info = mpa.plan_info(sh, seq_lens, qsl)
+    assert info.num_decode_seqs == 1 and info.num_prefill_seqs == 1
+    assert 9000 > info.split_tokens and info.split_tokens % 16 == 0
+    items = info.num_decode_items
+    assert items == -(-9000 // info.split_tokens)
+    assert n == items * 8 * (128 + 2) * 4
+    assert attention_rc(sh, seq_lens, qsl, ws=n - 1) == mpa.MPA_ERR_WORKSPACE
+
+
+def test_no_workspace_for_short_rows():
+    sh = shape()
+    assert mpa.workspace_size(sh, [40, 3], [0, 1, 5]) == 0
+
+
+def test_plan_info_counts():
+    sh = shape(num_seqs=5, total_q_tokens=1 + 1 + 70 + 0 + 2, max_blocks_per_seq=64)
+    seq_lens = [100, 1, 300, 50, 2]
+    qsl = [0, 1, 2, 72, 72, 74]
+    info = mpa.plan_info(sh, seq_lens, qsl)
+    assert info.num_decode_seqs == 2 and info.num_prefill_seqs == 2
+    # 64 (token, head) rows per tile: G = 4 -> 16 tokens per tile
+    assert info.num_prefill_tiles == (-(-70 // 16) + 1) * 2
+    assert info.decode_launches == 1
