@@ -1,0 +1,293 @@
+#!/usr/bin/env python3
+"""Throughput of one mixed prefill+decode attention step on one MI355X.
+
+A step is the whole hot path on one batch: mpa_kv_append, then the decode
+rows (split-K + merge) and the prefill chunks (causal MFMA tiles), all
+through the C ABI on one stream.  Inputs are synthetic and resident in HBM
+before timing starts.  Prints one JSON line:
+
+  value          query tokens/s over the timed steps (T * steps / wall time)
+  roofline       the dominant phase's algorithmic bytes (or FLOPs) per launch
+                 over its HIP-event-timed average duration, against the
+                 MI355X datasheet peak (HBM 8 TB/s, bf16 dense MFMA 2.5 PF)
+  cpu_baseline   the CPU oracle, timed on a bounded sample of the same step
+
+    python bench.py [--steps K] [--warmup W] [--config decode8b] [--seed 0]
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "mixed-step attention tokens/s; decode HBM GB/s and prefill MFMA % of peak"
+HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+MFMA_F32_PEAK_TFLOPS = 157.3
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_27085_amd", "csrc", "mpa_kernels.hip")
+
+WORKLOADS = {
+    "decode8b": "64 decode rows, ctx U{512..8192}; 32 q / 8 kv heads, head_dim 128, block 16, bf16",
+    "lent": "128 decode rows (ctx 1k-16k) + 2 prefill chunks of 2048 on prefixes 0-8k; 32/8/128, bf16",
+    "agentic": "256 decode rows (lognormal ctx, median 6k, cap 32k) + 4 chunks 512-4096 on 50-90% cached "
+               "4k-24k prompts; 64/8/128, bf16",
+    "budget0": "256 decode rows (ctx 4k-8k), no prefill; 32/8/128, bf16",
+    "budget256": "256 decode rows (ctx 4k-8k) + a 256-token chunk on a 4k prefix; 32/8/128, bf16",
+    "budget1024": "256 decode rows (ctx 4k-8k) + a 1024-token chunk on a 4k prefix; 32/8/128, bf16",
+    "budget4096": "256 decode rows (ctx 4k-8k) + a 4096-token chunk on a 4k prefix; 32/8/128, bf16",
+    "longctx": "32 decode rows (ctx 32k-128k) + one 8192-token chunk on a 64k prefix; 32/8/128, bf16",
+}
+
+
+def algorithmic_work(seq_lens, qsl, hq, hkv, d, elem_bytes, block=16):
+    """Bytes and FLOPs the step must move / compute at minimum.
+
+    decode row (context L):   K+V read 2*L*Hkv*d*e, q read + out write
+                              2*Hq*d*e, block ids 4*ceil(L/16)
+    prefill chunk (C on P):   K+V read 2*(P+C)*Hkv*d*e, q + out 2*C*Hq*d*e
+    append:                   new K/V read and written, 4*T*Hkv*d*e
+    FLOPs: 4*d*Hq per attended (query, key) pair; decode attends L pairs,
+    a chunk C*P + C*(C+1)/2."""
+    seq_lens = np.asarray(seq_lens, dtype=np.int64)
+    q_lens = np.diff(np.asarray(qsl, dtype=np.int64))
+    dec = q_lens == 1
+    pre = q_lens > 1
+    L = seq_lens
+    P = L - q_lens
+    C = q_lens
+    dec_bytes = int(np.sum((2 * L * hkv * d * elem_bytes + 2 * hq * d * elem_bytes + 4 * ((L + block - 1) // block))[dec]))
+    pre_bytes = int(np.sum((2 * L * hkv * d * elem_bytes + 2 * C * hq * d * elem_bytes)[pre]))
+    app_bytes = int(4 * q_lens.sum() * hkv * d * elem_bytes)
+    dec_flops = int(4 * d * hq * np.sum(L[dec]))
+    pre_flops = int(4 * d * hq * np.sum((C * P + C * (C + 1) // 2)[pre]))
+    return {
+        "decode_bytes": dec_bytes,
+        "prefill_bytes": pre_bytes,
+        "append_bytes": app_bytes,
+        "decode_flops": dec_flops,
+        "prefill_flops": pre_flops,
+        "decode_rows": int(dec.sum()),
+        "prefill_chunks": int(pre.sum()),
+        "query_tokens": int(q_lens.sum()),
+    }
+
+
+def kernel_source_sha() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(workload: str, phase: str):
+    """HBM bytes per launch from the committed rocprofv3 counter runs, or None
+    if there are none for this workload/phase or the kernels changed since."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f).get(workload, {}).get(phase)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("kernel_source_sha") != kernel_source_sha():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def blas_threads() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+
+        n = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
+        return max(n) if n else 1
+    except Exception:
+        return 1
+
+
+def cpu_baseline(d, budget_s: float, seed: int):
+    """Time the CPU oracle on a bounded, seeded sample of the step's rows.
+
+    Sequences are visited in a seeded order; a prefill chunk contributes up to
+    64 uniformly drawn rows.  Host copies of each sequence are made before its
+    timer starts.  Stops after the first sequence that takes the total past
+    ``budget_s`` (or after one full pass)."""
+    from oracle import ref
+    from workloads.device import host_subbatch
+
+    rng = np.random.default_rng(10_000 + seed)
+    order = rng.permutation(d.num_seqs)
+    rows_done = 0
+    elapsed = 0.0
+    seqs_done = 0
+    hkv, hd, bs = d.heads.num_kv_heads, d.heads.head_dim, d.heads.block_size
+    for s in order:
+        c = int(d.qsl_host[s + 1] - d.qsl_host[s])
+        if c == 0:
+            continue
+        sub = host_subbatch(d, [int(s)])["batch"]
+        rows = np.arange(c) if c <= 64 else np.sort(rng.choice(c, size=64, replace=False))
+        t0 = time.perf_counter()
+        prefix = int(sub.seq_lens[0]) - c
+        kp, vp = ref.gather_kv(sub.k_cache, sub.v_cache, sub.block_tables[0], prefix, hkv, hd, bs, sub.dtype)
+        k = np.concatenate([kp, ref.decode_raw(sub.k_new, sub.dtype)])
+        v = np.concatenate([vp, ref.decode_raw(sub.v_new, sub.dtype)])
+        ref.sequence_attention(ref.decode_raw(sub.q, sub.dtype), k, v, prefix, sub.scale, hkv, rows=rows)
+        elapsed += time.perf_counter() - t0
+        rows_done += len(rows)
+        seqs_done += 1
+        if elapsed >= budget_s:
+            break
+    return {
+        "value": rows_done / elapsed if elapsed > 0 else None,
+        "unit": "query tokens/s",
+        "cores": blas_threads(),
+        "kind": "oracle",
+        "sample": f"{rows_done} query rows of {seqs_done}/{d.num_seqs} sequences (seeded order; <=64 random rows "
+                  f"per prefill chunk), {elapsed:.1f} s of float64 numpy on {cpu_model()}, "
+                  f"{os.cpu_count()} logical CPUs visible",
+    }
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="decode8b", choices=sorted(WORKLOADS))
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args(argv)
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the attention step has no cross-GPU exchange and this build runs "
+              "on a single MI355X; run with --gpus 1.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2609_27085_amd as mpa
+    from workloads.configs import config_specs
+    from workloads.device import device_step
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    mpa.lib()
+    specs, heads, nb, rng = config_specs(args.config, args.seed)
+    d = device_step(specs, heads, "bf16", rng, args.seed, num_blocks=nb)
+    work = algorithmic_work(d.seq_lens_host, d.qsl_host, heads.num_q_heads, heads.num_kv_heads, heads.head_dim, 2)
+    ws = mpa.alloc_workspace(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.qsl_host, d.scale)
+    out = torch.empty_like(d.q)
+    lse = torch.empty(d.q.shape[:2], dtype=torch.float32, device=d.q.device)
+    stream = torch.cuda.current_stream()
+    has_dec = work["decode_rows"] > 0
+    has_pre = work["prefill_chunks"] > 0
+
+    def step(ev=None):
+        if ev:
+            ev[0].record(stream)
+        mpa.kv_append(d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
+                      d.seq_lens_host, d.qsl_host, stream=stream)
+        if ev:
+            ev[1].record(stream)
+        if has_dec:
+            mpa.decode_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
+                                 d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws, scale=d.scale,
+                                 stream=stream)
+        if ev:
+            ev[2].record(stream)
+        if has_pre:
+            mpa.prefill_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
+                                  d.seq_lens_host, d.qsl_host, out, lse=lse, scale=d.scale, stream=stream)
+        if ev:
+            ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(events[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    def avg_ms(a, b):
+        return float(np.mean([e[a].elapsed_time(e[b]) for e in events]))
+
+    phase_ms = {"append": avg_ms(0, 1), "decode": avg_ms(1, 2), "prefill": avg_ms(2, 3)}
+    ms_per_step = wall * 1e3 / args.steps
+    value = work["query_tokens"] * args.steps / wall
+    dec_gbs = work["decode_bytes"] / (phase_ms["decode"] * 1e-3) / 1e9 if has_dec else None
+    pre_tflops = work["prefill_flops"] / (phase_ms["prefill"] * 1e-3) / 1e12 if has_pre else None
+    # dominant phase: the one that takes longest
+    dom = "decode" if phase_ms["decode"] >= phase_ms["prefill"] else "prefill"
+    if dom == "decode":
+        achieved, peak, unit, bound = dec_gbs, HBM_PEAK_GBS, "GB/s", "hbm"
+        kernel = "decode_kernel+merge_kernel"
+    else:
+        achieved, peak, unit, bound = pre_tflops, MFMA_BF16_PEAK_TFLOPS, "TFLOP/s", "mfma"
+        kernel = "prefill_kernel"
+    roofline = {
+        "bound": bound,
+        "achieved": round(achieved, 2),
+        "peak": peak,
+        "unit": unit,
+        "frac": round(achieved / peak, 4),
+        "traffic": measured_traffic(args.config, dom),
+        "kernel": kernel,
+        "phase_ms": round(phase_ms[dom], 4),
+        "algorithmic_per_launch": work[f"{dom}_bytes"] if dom == "decode" else work["prefill_flops"],
+    }
+    total_bytes = work["decode_bytes"] + work["prefill_bytes"] + work["append_bytes"]
+    total_flops = work["decode_flops"] + work["prefill_flops"]
+    line = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "query tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) values, shuffled block tables)",
+        "config": {"workload": f"{args.config}: {WORKLOADS[args.config]}", "seed": args.seed,
+                   "decode_rows": work["decode_rows"], "prefill_chunks": work["prefill_chunks"],
+                   "query_tokens": work["query_tokens"], "parallelism": "single GPU"},
+        "roofline": roofline,
+        "phases_ms": {k: round(v, 4) for k, v in phase_ms.items()},
+        "decode_hbm_gbs": round(dec_gbs, 1) if dec_gbs else None,
+        "decode_hbm_frac": round(dec_gbs / HBM_PEAK_GBS, 4) if dec_gbs else None,
+        "prefill_tflops": round(pre_tflops, 2) if pre_tflops else None,
+        "prefill_mfma_frac": round(pre_tflops / MFMA_BF16_PEAK_TFLOPS, 4) if pre_tflops else None,
+        "step_hbm_gbs": round(total_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+        "step_attention_tflops": round(total_flops / (ms_per_step * 1e-3) / 1e12, 3),
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(d, args.cpu_seconds, args.seed)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

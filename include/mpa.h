@@ -93,7 +93,7 @@ typedef struct {
   int32_t num_blocks;         /* physical blocks in each cache */
   int32_t max_blocks_per_seq; /* row stride of block_tables */
   int32_t total_q_tokens;     /* T = query_start_loc[S] */
-  float scale;                /* softmax scale, e.g. 1/sqrt(d) */
+  float scale;                /* softmax scale, finite and > 0, e.g. 1/sqrt(d) */
   int32_t dtype;              /* mpa_dtype */
 } mpa_shape;
 
@@ -159,6 +159,27 @@ int mpa_mixed_paged_attention(const mpa_shape* shape, const void* q, const void*
                               const int32_t* seq_lens_host, const int32_t* query_start_loc_host,
                               const int32_t* block_tables_host, void* out, float* lse,
                               void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The two halves of mpa_mixed_paged_attention, for callers that time them
+ * separately or run them on two streams: mpa_decode_attention computes only
+ * the rows of sequences with q_len == 1 (split-K + merge; it alone needs the
+ * workspace), mpa_prefill_attention only the rows of sequences with
+ * q_len > 1.  Arguments and contracts are those of
+ * mpa_mixed_paged_attention; both halves read the whole batch's metadata, so
+ * running both gives results bit-identical to the mixed call.  The two
+ * write disjoint rows of out and lse and may run concurrently.
+ */
+int mpa_decode_attention(const mpa_shape* shape, const void* q, const void* k_cache, const void* v_cache,
+                         const int32_t* block_tables, const int32_t* seq_lens, const int32_t* query_start_loc,
+                         const int32_t* seq_lens_host, const int32_t* query_start_loc_host,
+                         const int32_t* block_tables_host, void* out, float* lse, void* workspace,
+                         size_t workspace_bytes, void* stream);
+
+int mpa_prefill_attention(const mpa_shape* shape, const void* q, const void* k_cache, const void* v_cache,
+                          const int32_t* block_tables, const int32_t* seq_lens, const int32_t* query_start_loc,
+                          const int32_t* seq_lens_host, const int32_t* query_start_loc_host,
+                          const int32_t* block_tables_host, void* out, float* lse, void* stream);
 
 /* Static description of a status code. */
 const char* mpa_status_string(int status);

@@ -105,25 +105,28 @@ def lse_merge(parts):
     return o, top + np.log(total)
 
 
-def sequence_attention(q_rows, k, v, prefix, scale, num_kv_heads, row_tile=512):
+def sequence_attention(q_rows, k, v, prefix, scale, num_kv_heads, row_tile=512, rows=None):
     """All query heads of one sequence.
 
     q_rows [C, Hq, d]; k, v [L, Hkv, d] with L = prefix + C.  Row i sits at
-    position prefix + i and sees keys 0 .. prefix + i."""
+    position prefix + i and sees keys 0 .. prefix + i.  ``rows`` (optional)
+    restricts the result to those row indices, in that order."""
     c, hq, d = q_rows.shape
     big_l = k.shape[0]
     g = hq // num_kv_heads
-    o = np.empty((c, hq, d))
-    lse = np.empty((c, hq))
+    rows = np.arange(c) if rows is None else np.asarray(rows)
+    n = len(rows)
+    o = np.empty((n, hq, d))
+    lse = np.empty((n, hq))
     keys = np.arange(big_l)
-    for r0 in range(0, c, row_tile):
-        r1 = min(c, r0 + row_tile)
-        visible = keys[None, :] <= (prefix + np.arange(r0, r1))[:, None]
+    kh = [np.ascontiguousarray(k[:, j]) for j in range(num_kv_heads)]
+    vh = [np.ascontiguousarray(v[:, j]) for j in range(num_kv_heads)]
+    for r0 in range(0, n, row_tile):
+        r1 = min(n, r0 + row_tile)
+        rr = rows[r0:r1]
+        visible = keys[None, :] <= (prefix + rr)[:, None]
         for h in range(hq):
-            kv = h // g
-            o[r0:r1, h], lse[r0:r1, h] = softmax_attention(
-                q_rows[r0:r1, h], k[:, kv], v[:, kv], scale, visible
-            )
+            o[r0:r1, h], lse[r0:r1, h] = softmax_attention(q_rows[rr, h], kh[h // g], vh[h // g], scale, visible)
     return o, lse
 
 

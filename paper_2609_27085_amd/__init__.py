@@ -38,6 +38,8 @@ EXPORTS = (
     "mpa_workspace_size",
     "mpa_status_string",
     "mpa_get_plan_info",
+    "mpa_decode_attention",
+    "mpa_prefill_attention",
 )
 
 
@@ -95,6 +97,10 @@ def lib() -> ctypes.CDLL:
         L.mpa_mixed_paged_attention.restype = ctypes.c_int
         L.mpa_mixed_paged_attention.argtypes = [
             _SHP, _P, _P, _P, _P, _P, _P, _I32P, _I32P, _I32P, _P, _P, _P, ctypes.c_size_t, _P]
+        L.mpa_decode_attention.restype = ctypes.c_int
+        L.mpa_decode_attention.argtypes = L.mpa_mixed_paged_attention.argtypes
+        L.mpa_prefill_attention.restype = ctypes.c_int
+        L.mpa_prefill_attention.argtypes = [_SHP, _P, _P, _P, _P, _P, _P, _I32P, _I32P, _I32P, _P, _P, _P]
         L.mpa_workspace_size.restype = ctypes.c_size_t
         L.mpa_workspace_size.argtypes = [_SHP, _I32P, _I32P]
         L.mpa_status_string.restype = ctypes.c_char_p
@@ -201,16 +207,37 @@ def kv_append(k_new, v_new, k_cache, v_cache, block_tables, seq_lens, query_star
         raise MpaError(rc, "mpa_kv_append")
 
 
-def mixed_paged_attention(q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host,
-                          out, lse=None, workspace=None, scale=None, block_tables_host=None, stream=None) -> None:
-    """mpa_mixed_paged_attention on torch device tensors."""
+def _attention(which, q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host, out,
+               lse, workspace, scale, block_tables_host, stream) -> None:
     sl, qs = _host_i32(seq_lens_host), _host_i32(qsl_host)
     bth = None if block_tables_host is None else _host_i32(block_tables_host)
     shape = shape_of(q, k_cache, block_tables, sl, scale)
-    ws_ptr, ws_bytes = (None, 0) if workspace is None else (_ptr(workspace), workspace.numel() * workspace.element_size())
-    rc = lib().mpa_mixed_paged_attention(
-        ctypes.byref(shape), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_tables), _ptr(seq_lens),
-        _ptr(query_start_loc), _i32p(sl), _i32p(qs), _i32p(bth), _ptr(out), _ptr(lse), ws_ptr, ws_bytes,
-        _stream(stream))
+    args = [ctypes.byref(shape), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_tables), _ptr(seq_lens),
+            _ptr(query_start_loc), _i32p(sl), _i32p(qs), _i32p(bth), _ptr(out), _ptr(lse)]
+    if which != "mpa_prefill_attention":
+        args += [None, 0] if workspace is None else [_ptr(workspace), workspace.numel() * workspace.element_size()]
+    args.append(_stream(stream))
+    rc = getattr(lib(), which)(*args)
     if rc != MPA_OK:
-        raise MpaError(rc, "mpa_mixed_paged_attention")
+        raise MpaError(rc, which)
+
+
+def mixed_paged_attention(q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host,
+                          out, lse=None, workspace=None, scale=None, block_tables_host=None, stream=None) -> None:
+    """mpa_mixed_paged_attention on torch device tensors."""
+    _attention("mpa_mixed_paged_attention", q, k_cache, v_cache, block_tables, seq_lens, query_start_loc,
+               seq_lens_host, qsl_host, out, lse, workspace, scale, block_tables_host, stream)
+
+
+def decode_attention(q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host,
+                     out, lse=None, workspace=None, scale=None, block_tables_host=None, stream=None) -> None:
+    """mpa_decode_attention: only the rows of sequences with q_len == 1."""
+    _attention("mpa_decode_attention", q, k_cache, v_cache, block_tables, seq_lens, query_start_loc,
+               seq_lens_host, qsl_host, out, lse, workspace, scale, block_tables_host, stream)
+
+
+def prefill_attention(q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host,
+                      out, lse=None, scale=None, block_tables_host=None, stream=None) -> None:
+    """mpa_prefill_attention: only the rows of sequences with q_len > 1."""
+    _attention("mpa_prefill_attention", q, k_cache, v_cache, block_tables, seq_lens, query_start_loc,
+               seq_lens_host, qsl_host, out, lse, None, scale, block_tables_host, stream)

@@ -25,6 +25,9 @@ HIPCC_FLAGS = [
     "-shared",
     # packed FP32 instructions stay off everywhere in this library
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in ordinary VGPRs: the softmax rescales them with VALU
+    # ops, and AGPR accumulators would be copied out and back every block
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wall",
     "-Wno-unused-result",
 ]

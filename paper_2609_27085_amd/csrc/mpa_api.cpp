@@ -26,7 +26,7 @@ struct Batch {
 int check_shape(const mpa_shape* sh) {
   if (!sh) return MPA_ERR_INVALID;
   if (sh->num_seqs < 0 || sh->num_q_heads <= 0 || sh->num_kv_heads <= 0 || sh->num_blocks < 0 ||
-      sh->max_blocks_per_seq < 0 || sh->total_q_tokens < 0 || !isfinite(sh->scale))
+      sh->max_blocks_per_seq < 0 || sh->total_q_tokens < 0 || !isfinite(sh->scale) || !(sh->scale > 0.f))
     return MPA_ERR_INVALID;
   if (sh->dtype != MPA_BF16 && sh->dtype != MPA_F32) return MPA_ERR_UNSUPPORTED;
   if (sh->head_dim != 64 && sh->head_dim != 128) return MPA_ERR_UNSUPPORTED;
@@ -70,19 +70,35 @@ int check_batch(const mpa_shape* sh, const int32_t* seq_lens, const int32_t* qsl
   return MPA_OK;
 }
 
-// KV tokens per decode split: enough (item, KV head) waves to fill the chip
-// several times over, in powers of two from 256 to 8192 tokens.  Overridable
-// with MPA_SPLIT_TOKENS (a multiple of 16) for tuning sweeps.
-int choose_split(const mpa_shape* sh, const Batch& b) {
+// KV tokens per decode split.  Every (split, KV head) is one wave, and a
+// wave's time is about proportional to its tokens plus a fixed start-up cost,
+// so the step takes about ceil(waves / slots) * (split + overhead), where
+// slots is the number of waves the device runs at once.  The split is the
+// multiple of 16 in [128, 1024] that minimises that estimate (more, smaller
+// splits fill the last round of waves; fewer, larger ones cut start-up and
+// merge work).  MPA_SPLIT_TOKENS (a multiple of 16, at most 1024) overrides
+// it for tuning sweeps.
+int choose_split(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens) {
   if (const char* env = getenv("MPA_SPLIT_TOKENS")) {
     const int v = atoi(env);
-    if (v >= kBlock && v % kBlock == 0) return v;
+    if (v >= kBlock && v <= 1024 && v % kBlock == 0) return v;
   }
-  const long target_waves = 256L * 32;  // 256 CUs, 32 waves each
-  int split = 256;
-  while (split < 8192 && (b.decode_tokens / split + (long)b.decode.size()) * sh->num_kv_heads > target_waves)
-    split *= 2;
-  return split;
+  if (b.decode.empty()) return 1024;
+  const long slots = mpa::decode_wave_slots(sh->dtype, sh->head_dim);
+  const long overhead = 64;
+  long best_cost = -1;
+  int best = 1024;
+  for (int split = 128; split <= 1024; split += kBlock) {
+    long items = 0;
+    for (int s : b.decode) items += std::max(1, (seq_lens[s] + split - 1) / split);
+    const long waves = items * sh->num_kv_heads;
+    const long cost = ((waves + slots - 1) / slots) * (split + overhead);
+    if (best_cost < 0 || cost < best_cost) {
+      best_cost = cost;
+      best = split;
+    }
+  }
+  return best;
 }
 
 long decode_items(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens, int split) {
@@ -92,7 +108,12 @@ long decode_items(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens, 
   return n;
 }
 
-int q_tile(const mpa_shape* sh) { return mpa::kPrefillRows / (sh->num_q_heads / sh->num_kv_heads); }
+// Query tokens per prefill tile: 128 (token, head) rows for the bf16 MFMA
+// kernel, 64 for the f32 kernel.
+int q_tile(const mpa_shape* sh) {
+  const int rows = sh->dtype == MPA_BF16 ? mpa::kPrefillRowsMfma : mpa::kPrefillRows;
+  return rows / (sh->num_q_heads / sh->num_kv_heads);
+}
 
 size_t workspace_bytes(const mpa_shape* sh, long items) {
   const size_t per = (size_t)sh->num_q_heads * (sh->head_dim + 2) * sizeof(float);
@@ -120,7 +141,7 @@ int mpa_get_plan_info(const mpa_shape* shape, const int32_t* seq_lens_host, cons
   Batch b;
   int rc = check_batch(shape, seq_lens_host, qsl_host, nullptr, false, &b);
   if (rc != MPA_OK) return rc;
-  const int split = choose_split(shape, b);
+  const int split = choose_split(shape, b, seq_lens_host);
   info->num_decode_seqs = (int32_t)b.decode.size();
   info->num_prefill_seqs = (int32_t)b.prefill.size();
   info->split_tokens = split;
@@ -136,7 +157,7 @@ int mpa_get_plan_info(const mpa_shape* shape, const int32_t* seq_lens_host, cons
 size_t mpa_workspace_size(const mpa_shape* shape, const int32_t* seq_lens_host, const int32_t* qsl_host) {
   Batch b;
   if (check_batch(shape, seq_lens_host, qsl_host, nullptr, false, &b) != MPA_OK) return 0;
-  const int split = choose_split(shape, b);
+  const int split = choose_split(shape, b, seq_lens_host);
   bool any_split = false;
   for (int s : b.decode) any_split |= seq_lens_host[s] > split;
   if (!any_split) return 0;
@@ -159,29 +180,59 @@ int mpa_kv_append(const mpa_shape* shape, const void* k_new, const void* v_new, 
   a.k_cache = k_cache;
   a.v_cache = v_cache;
   a.block_tables = block_tables;
-  a.seq_lens = seq_lens;
-  a.qsl = query_start_loc;
-  a.num_seqs = shape->num_seqs;
-  a.total_q = shape->total_q_tokens;
   a.hkv = shape->num_kv_heads;
   a.mb = shape->max_blocks_per_seq;
   a.nb = shape->num_blocks;
-  hipError_t e = mpa::launch_append(a, shape->dtype, shape->head_dim, (hipStream_t)stream);
-  return e == hipSuccess ? MPA_OK : MPA_ERR_HIP;
+  (void)seq_lens;
+  (void)query_start_loc;
+  std::vector<int> seqs(b.decode);
+  seqs.insert(seqs.end(), b.prefill.begin(), b.prefill.end());
+  for (size_t c0 = 0; c0 < seqs.size(); c0 += mpa::kMaxPlanSeqs) {
+    mpa::AppendPlan p;
+    memset(&p, 0, sizeof(p));
+    const size_t c1 = std::min(seqs.size(), c0 + mpa::kMaxPlanSeqs);
+    p.n_seqs = (int32_t)(c1 - c0);
+    int acc = 0;
+    for (size_t k = c0; k < c1; ++k) {
+      const int s = seqs[k];
+      const int ql = query_start_loc_host[s + 1] - query_start_loc_host[s];
+      p.seq[k - c0] = s;
+      p.row0[k - c0] = query_start_loc_host[s];
+      p.pos0[k - c0] = seq_lens_host[s] - ql;
+      p.tok_start[k - c0] = acc;
+      acc += ql;
+    }
+    p.tok_start[c1 - c0] = acc;
+    hipError_t e = mpa::launch_append(a, p, shape->dtype, shape->head_dim, (hipStream_t)stream);
+    if (e != hipSuccess) return MPA_ERR_HIP;
+  }
+  return MPA_OK;
 }
 
-int mpa_mixed_paged_attention(const mpa_shape* shape, const void* q, const void* k_cache, const void* v_cache,
-                              const int32_t* block_tables, const int32_t* seq_lens, const int32_t* query_start_loc,
-                              const int32_t* seq_lens_host, const int32_t* query_start_loc_host,
-                              const int32_t* block_tables_host, void* out, float* lse, void* workspace,
-                              size_t workspace_bytes_given, void* stream) {
+}  // extern "C"
+
+namespace {
+
+enum Phase { kDecode = 1, kPrefill = 2 };
+
+int run_attention(int phases, const mpa_shape* shape, const void* q, const void* k_cache, const void* v_cache,
+                  const int32_t* block_tables, const int32_t* seq_lens, const int32_t* query_start_loc,
+                  const int32_t* seq_lens_host, const int32_t* query_start_loc_host,
+                  const int32_t* block_tables_host, void* out, float* lse, void* workspace,
+                  size_t workspace_bytes_given, void* stream) {
   Batch b;
   int rc = check_batch(shape, seq_lens_host, query_start_loc_host, block_tables_host, false, &b);
   if (rc != MPA_OK) return rc;
+  if (!(phases & kDecode)) b.decode.clear();
+  if (!(phases & kPrefill)) b.prefill.clear();
   if (b.decode.empty() && b.prefill.empty()) return MPA_OK;
   if (!q || !k_cache || !v_cache || !block_tables || !seq_lens || !query_start_loc || !out)
     return MPA_ERR_INVALID;
-  const int split = choose_split(shape, b);
+  // The split size depends on every decode row of the batch, whichever
+  // phase runs, so that the phases together equal the mixed call exactly.
+  Batch all;
+  check_batch(shape, seq_lens_host, query_start_loc_host, nullptr, false, &all);
+  const int split = choose_split(shape, all, seq_lens_host);
   const long items = decode_items(shape, b, seq_lens_host, split);
   bool any_split = false;
   for (int s : b.decode) any_split |= seq_lens_host[s] > split;
@@ -189,7 +240,6 @@ int mpa_mixed_paged_attention(const mpa_shape* shape, const void* q, const void*
     const size_t need = workspace_bytes(shape, items);
     if (!workspace || workspace_bytes_given < need) return MPA_ERR_WORKSPACE;
   }
-
   mpa::AttnArgs a;
   a.q = q;
   a.k_cache = k_cache;
@@ -261,6 +311,38 @@ int mpa_mixed_paged_attention(const mpa_shape* shape, const void* q, const void*
     if (e != hipSuccess) return MPA_ERR_HIP;
   }
   return MPA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mpa_mixed_paged_attention(const mpa_shape* shape, const void* q, const void* k_cache, const void* v_cache,
+                              const int32_t* block_tables, const int32_t* seq_lens, const int32_t* query_start_loc,
+                              const int32_t* seq_lens_host, const int32_t* query_start_loc_host,
+                              const int32_t* block_tables_host, void* out, float* lse, void* workspace,
+                              size_t workspace_bytes_given, void* stream) {
+  return run_attention(kDecode | kPrefill, shape, q, k_cache, v_cache, block_tables, seq_lens, query_start_loc,
+                       seq_lens_host, query_start_loc_host, block_tables_host, out, lse, workspace,
+                       workspace_bytes_given, stream);
+}
+
+int mpa_decode_attention(const mpa_shape* shape, const void* q, const void* k_cache, const void* v_cache,
+                         const int32_t* block_tables, const int32_t* seq_lens, const int32_t* query_start_loc,
+                         const int32_t* seq_lens_host, const int32_t* query_start_loc_host,
+                         const int32_t* block_tables_host, void* out, float* lse, void* workspace,
+                         size_t workspace_bytes_given, void* stream) {
+  return run_attention(kDecode, shape, q, k_cache, v_cache, block_tables, seq_lens, query_start_loc,
+                       seq_lens_host, query_start_loc_host, block_tables_host, out, lse, workspace,
+                       workspace_bytes_given, stream);
+}
+
+int mpa_prefill_attention(const mpa_shape* shape, const void* q, const void* k_cache, const void* v_cache,
+                          const int32_t* block_tables, const int32_t* seq_lens, const int32_t* query_start_loc,
+                          const int32_t* seq_lens_host, const int32_t* query_start_loc_host,
+                          const int32_t* block_tables_host, void* out, float* lse, void* stream) {
+  return run_attention(kPrefill, shape, q, k_cache, v_cache, block_tables, seq_lens, query_start_loc,
+                       seq_lens_host, query_start_loc_host, block_tables_host, out, lse, nullptr, 0, stream);
 }
 
 }  // extern "C"

@@ -11,7 +11,8 @@ namespace mpa {
 constexpr int kBlock = 16;            // tokens per cache block
 constexpr int kWavesPerGroup = 4;     // waves per workgroup in every kernel
 constexpr int kMaxPlanSeqs = 256;     // sequences per launch (kernel-argument plan)
-constexpr int kPrefillRows = 64;      // (token, head) rows per prefill workgroup
+constexpr int kPrefillRows = 64;      // (token, head) rows per f32 prefill workgroup
+constexpr int kPrefillRowsMfma = 128; // (token, head) rows per bf16 prefill workgroup
 
 // Pointers and sizes common to the attention kernels.
 struct AttnArgs {
@@ -56,14 +57,25 @@ struct AppendArgs {
   void* k_cache;
   void* v_cache;
   const int32_t* block_tables;
-  const int32_t* seq_lens;
-  const int32_t* qsl;
-  int32_t num_seqs, total_q, hkv, mb, nb;
+  int32_t hkv, mb, nb;
+};
+
+// Append work for up to kMaxPlanSeqs sequences: token k of this launch is new
+// token (k - tok_start[j]) of sequence seq[j]; that token is query row
+// row0[j] + (k - tok_start[j]) at position pos0[j] + (k - tok_start[j]).
+struct AppendPlan {
+  int32_t n_seqs;
+  int32_t seq[kMaxPlanSeqs];
+  int32_t row0[kMaxPlanSeqs];
+  int32_t pos0[kMaxPlanSeqs];
+  int32_t tok_start[kMaxPlanSeqs + 1];
 };
 
 // Launchers (mpa_kernels.hip).  dtype: 0 = bf16, 1 = f32.  Return the HIP
 // error of the launch.
-hipError_t launch_append(const AppendArgs& a, int dtype, int head_dim, hipStream_t stream);
+hipError_t launch_append(const AppendArgs& a, const AppendPlan& p, int dtype, int head_dim, hipStream_t stream);
+// Decode waves the current device holds at once (2048 without a device).
+int decode_wave_slots(int dtype, int head_dim);
 hipError_t launch_decode(const AttnArgs& a, const DecodePlan& p, int n_items, int dtype, int head_dim,
                          hipStream_t stream);
 hipError_t launch_merge(const AttnArgs& a, const DecodePlan& p, int dtype, int head_dim, hipStream_t stream);

@@ -25,6 +25,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "mpa_internal.h"
 
 namespace mpa {
@@ -139,67 +141,129 @@ __device__ inline int upper_index(const int32_t* starts, int n, int x) {
 // n) against cache blocks kb_begin .. kb_end-1 of one sequence and KV head.
 // Key `key` is visible to row n iff key <= limit (per lane) and key < kend;
 // V rows of keys >= kend are replaced by zero (they may hold NaN/Inf).
+//
+// The loop is software-pipelined one block deep: block kb+1's K and V
+// fragments are in flight while block kb is consumed.  Block ids come from a
+// coalesced load of up to 64 consecutive block-table entries, one per lane,
+// and are broadcast with readlane.
 template <int DT, int D>
 struct RowState {
   f32x4 acc[D / 16];
-  float m;  // running max, log2 units
-  float l;  // this lane's part of the running sum
+  float m;  // reference maximum of the row's scaled scores (log2 units)
+  float l;  // this lane's part of the running sum of 2^(s*c - m)
 };
 
 template <int DT, int D>
-__device__ inline void attend_blocks(const AttnArgs& a, const typename Tr<DT>::Chunk* qf,
-                                     const int32_t* bt, int g, int kb_begin, int kb_end, int kend,
-                                     int limit, RowState<DT, D>& st, bool& poison) {
+struct BlockFrags {
+  typename Tr<DT>::Chunk k[D / (4 * Tr<DT>::X)];
+  typename Tr<DT>::VFrag v[D / 16];
+};
+
+template <int DT, int D>
+__device__ inline void load_block(const AttnArgs& a, int blk, int g, BlockFrags<DT, D>& f) {
   using T = Tr<DT>;
   using E = typename T::Elem;
   constexpr int X = T::X;
-  constexpr int R = D / (4 * X);
-  constexpr int MT = D / 16;
   const int lane = threadIdx.x & 63;
   const int n = lane & 15, grp = lane >> 4;
-  const size_t granule = (size_t)D * kBlock;
-  for (int kb = kb_begin; kb < kb_end; ++kb) {
-    int blk = bt[kb];
-    if (blk < 0 || blk >= a.nb) {
-      poison = true;
-      blk = 0;
-    }
-    const size_t base = ((size_t)blk * a.hkv + g) * granule;
-    const E* kp = reinterpret_cast<const E*>(a.k_cache) + base;
-    const E* vp = reinterpret_cast<const E*>(a.v_cache) + base;
-    f32x4 s = {0.f, 0.f, 0.f, 0.f};
+  const size_t base = ((size_t)blk * a.hkv + g) * ((size_t)D * kBlock);
+  const E* kp = reinterpret_cast<const E*>(a.k_cache) + base;
+  const E* vp = reinterpret_cast<const E*>(a.v_cache) + base;
 #pragma unroll
-    for (int r = 0; r < R; ++r) s = T::qk(T::load_chunk(kp + ((4 * r + grp) * kBlock + n) * X), qf[r], s);
-    typename T::VFrag vf[MT];
+  for (int r = 0; r < D / (4 * X); ++r) f.k[r] = T::load_chunk(kp + ((4 * r + grp) * kBlock + n) * X);
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) vf[mt] = T::load_v(vp + (16 * mt + n) * kBlock + 4 * grp);
-    const int key0 = kb * kBlock + 4 * grp;
-    float s2[4];
-    float bm = -INFINITY;
+  for (int mt = 0; mt < D / 16; ++mt) f.v[mt] = T::load_v(vp + (16 * mt + n) * kBlock + 4 * grp);
+}
+
+// Scores -> probabilities -> PV for one 16-key block.  Scores are scaled to
+// log2 units first (s2 = s * scale * log2(e)).  The softmax keeps a lazily
+// moved reference maximum m per row: probabilities are 2^(s2 - m), and m
+// (with the O / l rescale it implies) only moves when some score of the wave
+// exceeds it by more than 8, so probabilities stay <= 2^8 and the
+// accumulators are rescaled on a few blocks only.  The quotient O / l at the
+// end is the same for any m; the block that sets m has its maximum at
+// exactly 2^0 = 1, so a single key returns its value row unchanged.
+// `edge` (wave-uniform) marks a block with keys past kend or past some row's
+// causal limit; only then are scores masked and V rows of keys >= kend zeroed.
+template <int DT, int D>
+__device__ inline void consume_block(const AttnArgs& a, const typename Tr<DT>::Chunk* qf, const BlockFrags<DT, D>& f,
+                                     int kb, int kend, int limit, bool edge, RowState<DT, D>& st) {
+  using T = Tr<DT>;
+  constexpr int R = D / (4 * T::X);
+  constexpr int MT = D / 16;
+  const int grp = (threadIdx.x & 63) >> 4;
+  f32x4 s = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int key = key0 + i;
-      s2[i] = (key <= limit && key < kend) ? s[i] * a.scale_log2 : -INFINITY;
-      bm = fmaxf(bm, s2[i]);
-    }
-    bm = fmaxf(bm, __shfl_xor(bm, 16));
+  for (int r = 0; r < R; ++r) s = T::qk(f.k[r], qf[r], s);
+  s *= a.scale_log2;
+  const int key0 = kb * kBlock + 4 * grp;
+  if (edge) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (!(key0 + i <= limit && key0 + i < kend)) s[i] = -INFINITY;
+  }
+  const float lmax = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
+  if (__any(lmax > st.m + 8.f)) {
+    float bm = fmaxf(lmax, __shfl_xor(lmax, 16));
     bm = fmaxf(bm, __shfl_xor(bm, 32));
     const float m_new = fmaxf(st.m, bm);
-    // A row with no visible key so far keeps m = -inf; use 0 as the pivot
-    // so that exp2 sees -inf - 0 = -inf rather than -inf - -inf = NaN.
-    const float pivot = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = exp2_fast(st.m - pivot);
-    f32x4 p;
+    const float alpha = m_new == -INFINITY ? 1.f : exp2_fast(st.m - m_new);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) p[i] = exp2_fast(s2[i] - pivot);
-    st.l = st.l * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
+    for (int mt = 0; mt < MT; ++mt) st.acc[mt] *= alpha;
+    st.l *= alpha;
     st.m = m_new;
-    const auto pf = T::make_p(p);
+  }
+  // rows whose reference is still -inf have seen no visible key: p = 0
+  const float m = st.m == -INFINITY ? 0.f : st.m;
+  f32x4 p;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) p[i] = exp2_fast(s[i] - m);
+  st.l += (p[0] + p[1]) + (p[2] + p[3]);
+  const auto pf = T::make_p(p);
+  if (edge) {
     const int nvalid = kend - key0;
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const auto v = nvalid < 4 ? T::keep_first(vf[mt], nvalid) : vf[mt];
-      st.acc[mt] = T::pv(v, pf, st.acc[mt] * alpha);
+    for (int mt = 0; mt < MT; ++mt) st.acc[mt] = T::pv(T::keep_first(f.v[mt], nvalid), pf, st.acc[mt]);
+  } else {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) st.acc[mt] = T::pv(f.v[mt], pf, st.acc[mt]);
+  }
+}
+
+// Blocks kb_begin .. kb_end-1 for 16 rows whose smallest causal limit is
+// min_limit.  Software-pipelined one block deep: the next block's fragments
+// are requested before the current one is consumed (the request is pinned
+// in place with a scheduling barrier, and is issued unconditionally -- the
+// last block is requested twice -- so consuming a block waits only for its
+// own loads).  Block ids come from a coalesced load of up to 64 consecutive
+// block-table entries, one per lane, broadcast with readlane.
+template <int DT, int D>
+__device__ inline void attend_blocks(const AttnArgs& a, const typename Tr<DT>::Chunk* qf,
+                                     const int32_t* bt, int g, int kb_begin, int kb_end, int kend,
+                                     int limit, int min_limit, RowState<DT, D>& st, bool& poison) {
+  const int lane = threadIdx.x & 63;
+  for (int c0 = kb_begin; c0 < kb_end; c0 += 64) {
+    const int c1 = min(kb_end, c0 + 64);
+    const int ids = c0 + lane < c1 ? bt[c0 + lane] : 0;
+    auto block_id = [&](int kb) -> int {
+      int blk = __builtin_amdgcn_readlane(ids, kb - c0);
+      if (blk < 0 || blk >= a.nb) {
+        poison = true;
+        blk = 0;
+      }
+      return blk;
+    };
+    auto is_edge = [&](int kb) { return kb * kBlock + kBlock > kend || kb * kBlock + kBlock - 1 > min_limit; };
+    BlockFrags<DT, D> fa, fb;
+    load_block<DT, D>(a, block_id(c0), g, fa);
+    for (int kb = c0; kb < c1; kb += 2) {
+      load_block<DT, D>(a, block_id(min(kb + 1, c1 - 1)), g, fb);
+      __builtin_amdgcn_sched_barrier(0);
+      consume_block<DT, D>(a, qf, fa, kb, kend, limit, is_edge(kb), st);
+      if (kb + 1 >= c1) break;
+      load_block<DT, D>(a, block_id(min(kb + 2, c1 - 1)), g, fa);
+      __builtin_amdgcn_sched_barrier(0);
+      consume_block<DT, D>(a, qf, fb, kb + 1, kend, limit, is_edge(kb + 1), st);
     }
   }
 }
@@ -245,7 +309,7 @@ __global__ __launch_bounds__(256) void decode_kernel(AttnArgs a, DecodePlan p) {
   st.l = 0.f;
   bool poison = false;
   attend_blocks<DT, D>(a, qf, a.block_tables + (size_t)s * a.mb, g, k0 / kBlock,
-                       (k1 + kBlock - 1) / kBlock, k1, INT32_MAX, st, poison);
+                       (k1 + kBlock - 1) / kBlock, k1, INT32_MAX, INT32_MAX, st, poison);
 
   float l = st.l + __shfl_xor(st.l, 16);
   l += __shfl_xor(l, 32);
@@ -272,12 +336,16 @@ __global__ __launch_bounds__(256) void decode_kernel(AttnArgs a, DecodePlan p) {
 // Split-K merge: one 64-lane workgroup per (decode sequence, query head).
 // With split maxima m_j and sums l_j (log2 units), the row's softmax
 // denominator is sum_j l_j 2^(m_j - M) with M = max_j m_j, and its output is
-// sum_j acc_j 2^(m_j - M) divided by that denominator.
+// sum_j acc_j 2^(m_j - M) divided by that denominator.  Lanes load the
+// (m_j, l_j) of 64 splits at once; the weights go through LDS and every lane
+// then accumulates D/64 output dims over the splits with independent loads.
 template <int DT, int D>
 __global__ __launch_bounds__(64) void merge_kernel(AttnArgs a, DecodePlan p) {
   using T = Tr<DT>;
   using E = typename T::Elem;
   constexpr int PER = D / 64;
+  __shared__ float w_s[64];
+  const int lane = threadIdx.x;
   const int j = blockIdx.x;
   const int h = blockIdx.y;
   if (j >= p.n_seqs) return;
@@ -286,24 +354,42 @@ __global__ __launch_bounds__(64) void merge_kernel(AttnArgs a, DecodePlan p) {
   const int s = p.seq[j];
   const size_t base = (size_t)p.item_base + p.item_start[j];
   float M = -INFINITY;
-  for (int i = 0; i < n; ++i) M = fmaxf(M, a.ws_ml[((base + i) * a.hq + h) * 2]);
+  for (int i = lane; i < n; i += 64) M = fmaxf(M, a.ws_ml[((base + i) * a.hq + h) * 2]);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
   float lsum = 0.f;
   float o[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) o[e] = 0.f;
-  for (int i = 0; i < n; ++i) {
-    const size_t slot = (base + i) * a.hq + h;
-    const float w = exp2_fast(a.ws_ml[slot * 2] - M);
-    lsum += w * a.ws_ml[slot * 2 + 1];
+  for (int c0 = 0; c0 < n; c0 += 64) {
+    const int i = c0 + lane;
+    float w = 0.f;
+    if (i < n) {
+      const size_t slot = (base + i) * a.hq + h;
+      w = exp2_fast(a.ws_ml[slot * 2] - M);
+      lsum += w * a.ws_ml[slot * 2 + 1];
+    }
+    __syncthreads();
+    w_s[lane] = w;
+    __syncthreads();
+    const int cnt = min(64, n - c0);
+    const float* acc = a.ws_o + ((base + c0) * a.hq + h) * D + lane;
+    const size_t stride = (size_t)a.hq * D;
+#pragma unroll 8
+    for (int k = 0; k < cnt; ++k) {
+      const float wk = w_s[k];
 #pragma unroll
-    for (int e = 0; e < PER; ++e) o[e] += w * a.ws_o[slot * D + threadIdx.x + 64 * e];
+      for (int e = 0; e < PER; ++e) o[e] += wk * acc[k * stride + 64 * e];
+    }
   }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) lsum += __shfl_xor(lsum, off);
   const int t = a.qsl[s];
   E* out = reinterpret_cast<E*>(a.out) + ((size_t)t * a.hq + h) * D;
   const float inv = 1.f / lsum;
 #pragma unroll
-  for (int e = 0; e < PER; ++e) T::store1(out + threadIdx.x + 64 * e, o[e] * inv);
-  if (a.lse && threadIdx.x == 0) a.lse[(size_t)t * a.hq + h] = (M + log2f(lsum)) * kLn2;
+  for (int e = 0; e < PER; ++e) T::store1(out + lane + 64 * e, o[e] * inv);
+  if (a.lse && lane == 0) a.lse[(size_t)t * a.hq + h] = (M + log2f(lsum)) * kLn2;
 }
 
 // ---------------------------------------------------------------------------
@@ -352,8 +438,9 @@ __global__ __launch_bounds__(256) void prefill_kernel(AttnArgs a, PrefillPlan p)
   st.m = -INFINITY;
   st.l = 0.f;
   bool poison = false;
+  const int min_limit = P + min(first_tok + (wave * 16) / G, C - 1);
   attend_blocks<DT, D>(a, qf, a.block_tables + (size_t)s * a.mb, g, 0, (kend + kBlock - 1) / kBlock,
-                       kend, P + i, st, poison);
+                       kend, P + i, min_limit, st, poison);
 
   float l = st.l + __shfl_xor(st.l, 16);
   l += __shfl_xor(l, 32);
@@ -362,38 +449,284 @@ __global__ __launch_bounds__(256) void prefill_kernel(AttnArgs a, PrefillPlan p)
   E* o = reinterpret_cast<E*>(a.out) + ((size_t)(t0 + i) * a.hq + h) * D;
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) T::store4(o + 16 * mt + 4 * grp, st.acc[mt] * inv);
-  if (a.lse && grp == 0) a.lse[(size_t)(t0 + i) * a.hq + h] = poison ? NAN : (st.m + log2f(l)) * kLn2;
+  if (a.lse && grp == 0)
+    a.lse[(size_t)(t0 + i) * a.hq + h] = poison ? NAN : (st.m + log2f(l)) * kLn2;
 }
 
 // ---------------------------------------------------------------------------
-// Append: one thread per 16-byte chunk of one new (token, KV head) key row;
-// the same thread copies the matching X value elements.
+// Prefill chunks, bf16: the tensor-core path.  One workgroup of 4 waves per
+// (sequence, 128-row query tile, KV head); row r of the tile is token r / G
+// and head r % G of the group, so the G heads that share a KV head share
+// every K/V tile.  Each wave owns 32 rows (one 32-wide MFMA column tile).
+//
+// Per 64-key tile (4 cache blocks), staged in LDS and double-buffered:
+//   S^T[64 keys][32 rows] = K . Q^T   2 x (D/16) v_mfma_f32_32x32x16_bf16
+//   O^T[D][32 rows]     += V^T . P^T  (D/32) x 4 v_mfma_f32_32x32x16_bf16
+// K is copied to LDS verbatim (a block is [D/8 chunks][16 keys][8]); each
+// 16-key row of V^T is copied with its 4-key groups 1 and 2 swapped, so that
+// the 8 keys one lane feeds the PV product (keys 4h..4h+3 and 8+4h..8+4h+3 of
+// a block, from the 32x32 output layout of S^T) are 16 contiguous bytes.
+//
+// Softmax: exact online softmax with a lazily updated reference maximum.  The
+// running reference m only moves when a row's new maximum exceeds it by more
+// than 8 (log2 units), so exp2(s - m) <= 2^8 and the O / l rescale is skipped
+// for almost every tile; the final O / l is the same quotient either way.
+template <int D>
+__global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(AttnArgs a, PrefillPlan p) {
+  using f32x16 = float __attribute__((ext_vector_type(16)));
+  constexpr int BN = 64;                 // keys per tile
+  constexpr int NB = BN / kBlock;        // cache blocks per tile
+  constexpr int BLK = kBlock * D;        // elements of one (block, head) granule
+  constexpr int KS = D / 16;             // k-steps of the QK^T product
+  constexpr int DT = D / 32;             // 32-dim row tiles of O^T
+  constexpr int KCH = NB * BLK / 8 / 256;  // 16-byte K chunks each thread copies
+  constexpr int VR = NB * D / 256;         // 32-byte V^T rows each thread copies
+  static_assert(KCH >= 1 && VR >= 1, "tile copy shape");
+  __shared__ __attribute__((aligned(16))) uint16_t sk[2][NB * BLK];
+  __shared__ __attribute__((aligned(16))) uint16_t sv[2][NB * BLK];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = wave_uniform(tid >> 6);
+  const int n_tiles = p.tile_start[p.n_seqs];
+  const int g = blockIdx.x % a.hkv;
+  const int tile = n_tiles - 1 - (int)(blockIdx.x / a.hkv);  // last (longest) query tiles first
+  const int j = upper_index(p.tile_start, p.n_seqs, tile);
+  const int s = p.seq[j];
+  const int qt = tile - p.tile_start[j];
+  const int t0 = a.qsl[s];
+  const int C = a.qsl[s + 1] - t0;
+  const int L = a.seq_lens[s];
+  const int P = L - C;
+  const int G = a.hq / a.hkv;
+  const int first_tok = qt * p.q_tile;
+  const int last_tok = min(first_tok + p.q_tile - 1, C - 1);
+  const int kend = P + last_tok + 1;  // keys the workgroup needs
+  const int ntile = (kend + BN - 1) / BN;
+  const int32_t* bt = a.block_tables + (size_t)s * a.mb;
+
+  // this lane's query row
+  const int n = lane & 31, h = lane >> 5;
+  const int row = wave * 32 + n;
+  const int i_raw = first_tok + row / G;
+  const bool row_ok = i_raw < C;
+  const int i = row_ok ? i_raw : C - 1;
+  const int head = g * G + row % G;
+  const int limit = P + i;
+  const int w_first = first_tok + (wave * 32) / G;
+  const bool wave_active = w_first < C;
+  const int w_min_limit = P + min(w_first, C - 1);
+  const int w_kend = P + min(first_tok + (wave * 32 + 31) / G, C - 1) + 1;
+
+  bf16x8 qf[KS];
+  {
+    const uint16_t* q = reinterpret_cast<const uint16_t*>(a.q) + ((size_t)(t0 + i) * a.hq + head) * D;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      qf[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(q + (2 * ks + h) * 8));
+  }
+
+  // ---- global -> registers -> LDS tile copy
+  u32x4 kreg[KCH];
+  u32x4 vreg[VR][2];
+  auto load_tile = [&](int kt) {
+#pragma unroll
+    for (int u = 0; u < KCH; ++u) {
+      const int ci = tid + 256 * u;
+      const int bi = ci / (BLK / 8);
+      const int kb = kt * NB + bi;
+      u32x4 val = {0u, 0u, 0u, 0u};
+      if (kb * kBlock < kend) {
+        int blk = bt[kb];
+        if (blk >= 0 && blk < a.nb)
+          val = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(a.k_cache) +
+                                                ((size_t)blk * a.hkv + g) * BLK + (ci % (BLK / 8)) * 8);
+      }
+      kreg[u] = val;
+    }
+#pragma unroll
+    for (int u = 0; u < VR; ++u) {
+      const int ri = tid + 256 * u;
+      const int bi = ri / D;
+      const int d = ri % D;
+      const int kb = kt * NB + bi;
+      u32x4 lo = {0u, 0u, 0u, 0u}, hi = {0u, 0u, 0u, 0u};
+      if (kb * kBlock < kend) {
+        int blk = bt[kb];
+        if (blk >= 0 && blk < a.nb) {
+          const uint16_t* src =
+              reinterpret_cast<const uint16_t*>(a.v_cache) + ((size_t)blk * a.hkv + g) * BLK + d * kBlock;
+          lo = *reinterpret_cast<const u32x4*>(src);
+          hi = *reinterpret_cast<const u32x4*>(src + 8);
+          // keys >= L of the sequence's last block may hold NaN/Inf: zero them
+          const int nvalid = L - kb * kBlock;
+          if (nvalid < kBlock) {
+#pragma unroll
+            for (int w = 0; w < 8; ++w) {
+              const int k0 = 2 * w;
+              unsigned int word = w < 4 ? lo[w] : hi[w - 4];
+              word = k0 >= nvalid ? 0u : (k0 + 1 >= nvalid ? (word & 0xFFFFu) : word);
+              if (w < 4) lo[w] = word; else hi[w - 4] = word;
+            }
+          }
+        } else {
+          const u32x4 nan2 = {0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u};
+          lo = nan2;  // an invalid block id poisons the rows that read this tile
+          hi = nan2;
+        }
+      }
+      vreg[u][0] = lo;
+      vreg[u][1] = hi;
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < KCH; ++u) {
+      const int ci = tid + 256 * u;
+      *reinterpret_cast<u32x4*>(&sk[buf][ci * 8]) = kreg[u];
+    }
+#pragma unroll
+    for (int u = 0; u < VR; ++u) {
+      const int ri = tid + 256 * u;
+      const u32x4 lo = vreg[u][0], hi = vreg[u][1];
+      const u32x4 a0 = {lo[0], lo[1], hi[0], hi[1]};  // keys 0-3, 8-11
+      const u32x4 a1 = {lo[2], lo[3], hi[2], hi[3]};  // keys 4-7, 12-15
+      *reinterpret_cast<u32x4*>(&sv[buf][ri * kBlock]) = a0;
+      *reinterpret_cast<u32x4*>(&sv[buf][ri * kBlock + 8]) = a1;
+    }
+  };
+
+  f32x16 o[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[dt][r] = 0.f;
+  const float c = a.scale_log2;
+  const float thresh = 8.f / c;  // 8 in log2 units, in raw score units
+  float m_ref = -INFINITY;       // reference maximum, raw score units
+  float l = 0.f;
+
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+  for (int kt = 0; kt < ntile; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < ntile) load_tile(kt + 1);
+    const int key_base = kt * BN;
+    if (wave_active && key_base < w_kend) {
+      const uint16_t* K = sk[buf];
+      const uint16_t* V = sv[buf];
+      f32x16 st[2];
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) st[rt][r] = 0.f;
+        const uint16_t* kbase = K + (2 * rt + (n >> 4)) * BLK + (n & 15) * 8;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8 kf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kbase + (2 * ks + h) * 128));
+          st[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], st[rt], 0, 0, 0);
+        }
+      }
+      if (key_base + BN - 1 > w_min_limit) {
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = key_base + 32 * rt + 8 * (r >> 2) + 4 * h + (r & 3);
+            if (key > limit) st[rt][r] = -INFINITY;
+          }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[rt][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      if (__any(mx > m_ref + thresh)) {
+        const float m_new = fmaxf(m_ref, mx);
+        const float alpha = m_new == -INFINITY ? 1.f : exp2_fast((m_ref - m_new) * c);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+        l *= alpha;
+        m_ref = m_new;
+      }
+      const float mc = m_ref * c;
+      bf16x8 pb[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float pv = exp2_fast(fmaf(st[t >> 1][8 * (t & 1) + e], c, -mc));
+          l += pv;
+          pb[t][e] = (__bf16)pv;
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const uint16_t* vbase = V + t * BLK + n * kBlock + 8 * h;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          const bf16x8 vf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(vbase + 32 * dt * kBlock));
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[t], o[dt], 0, 0, 0);
+        }
+      }
+    }
+    if (kt + 1 < ntile) store_tile(buf ^ 1);
+    __syncthreads();
+  }
+
+  const float lt = l + __shfl_xor(l, 32);
+  if (!wave_active || !row_ok) return;
+  const float inv = 1.f / lt;
+  uint16_t* out = reinterpret_cast<uint16_t*>(a.out) + ((size_t)(t0 + i) * a.hq + head) * D;
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int jb = 0; jb < 4; ++jb) {
+      f32x4 v4 = {o[dt][4 * jb], o[dt][4 * jb + 1], o[dt][4 * jb + 2], o[dt][4 * jb + 3]};
+      Tr<0>::store4(out + 32 * dt + 8 * jb + 4 * h, v4 * inv);
+    }
+  if (a.lse && h == 0) a.lse[(size_t)(t0 + i) * a.hq + head] = (m_ref * c + log2f(lt)) * kLn2;
+}
+
+// ---------------------------------------------------------------------------
+// Append: one wave per new token.  The token's sequence comes from the
+// kernel-argument plan (a scalar binary search), its block id from one scalar
+// load; the wave then copies the token's Hkv*d key elements as 16-byte
+// chunks and its value elements into the V^T rows of the slot.
 template <int DT, int D>
-__global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
+__global__ __launch_bounds__(256) void append_kernel(AppendArgs a, AppendPlan p) {
   using T = Tr<DT>;
   using E = typename T::Elem;
   constexpr int X = T::X;
   constexpr int NC = D / X;
-  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
-  const long total = (long)a.total_q * a.hkv * NC;
-  if (idx >= total) return;
-  const int c = (int)(idx % NC);
-  const long th = idx / NC;
-  const int h = (int)(th % a.hkv);
-  const int t = (int)(th / a.hkv);
-  const int s = upper_index(a.qsl, a.num_seqs, t);
-  const int pos = a.seq_lens[s] - (a.qsl[s + 1] - a.qsl[s]) + (t - a.qsl[s]);
+  const int lane = threadIdx.x & 63;
+  const int tok = blockIdx.x * kWavesPerGroup + wave_uniform(threadIdx.x >> 6);
+  if (tok >= p.tok_start[p.n_seqs]) return;
+  const int j = upper_index(p.tok_start, p.n_seqs, tok);
+  const int k = tok - p.tok_start[j];
+  const int s = p.seq[j];
+  const int t = p.row0[j] + k;
+  const int pos = p.pos0[j] + k;
   const int blk = a.block_tables[(size_t)s * a.mb + pos / kBlock];
   if (blk < 0 || blk >= a.nb) return;
   const int slot = pos % kBlock;
-  const size_t head = (size_t)blk * a.hkv + h;
-  const E* kn = reinterpret_cast<const E*>(a.k_new) + ((size_t)t * a.hkv + h) * D + c * X;
-  E* kc = reinterpret_cast<E*>(a.k_cache) + ((head * NC + c) * kBlock + slot) * X;
-  *reinterpret_cast<u32x4*>(kc) = *reinterpret_cast<const u32x4*>(kn);
-  const E* vn = reinterpret_cast<const E*>(a.v_new) + ((size_t)t * a.hkv + h) * D + c * X;
-  E* vc = reinterpret_cast<E*>(a.v_cache) + (head * D + c * X) * kBlock + slot;
+  for (int ci = lane; ci < a.hkv * NC; ci += 64) {
+    const int h = ci / NC;
+    const int c = ci - h * NC;
+    const size_t head = (size_t)blk * a.hkv + h;
+    const E* kn = reinterpret_cast<const E*>(a.k_new) + ((size_t)t * a.hkv + h) * D + c * X;
+    E* kc = reinterpret_cast<E*>(a.k_cache) + ((head * NC + c) * kBlock + slot) * X;
+    *reinterpret_cast<u32x4*>(kc) = *reinterpret_cast<const u32x4*>(kn);
+    const E* vn = reinterpret_cast<const E*>(a.v_new) + ((size_t)t * a.hkv + h) * D + c * X;
+    E* vc = reinterpret_cast<E*>(a.v_cache) + (head * D + c * X) * kBlock + slot;
+    E vv[X];
 #pragma unroll
-  for (int e = 0; e < X; ++e) vc[e * kBlock] = vn[e];
+    for (int e = 0; e < X; ++e) vv[e] = vn[e];
+#pragma unroll
+    for (int e = 0; e < X; ++e) vc[e * kBlock] = vv[e];
+  }
 }
 
 template <template <int, int> class F, typename... Args>
@@ -407,10 +740,11 @@ hipError_t dispatch(int dtype, int head_dim, Args&&... args) {
 
 template <int DT, int D>
 struct AppendL {
-  static hipError_t run(const AppendArgs& a, hipStream_t stream) {
-    const long total = (long)a.total_q * a.hkv * (D / Tr<DT>::X);
-    if (total == 0) return hipSuccess;
-    hipLaunchKernelGGL((append_kernel<DT, D>), dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream, a);
+  static hipError_t run(const AppendArgs& a, const AppendPlan& p, hipStream_t stream) {
+    const int tokens = p.tok_start[p.n_seqs];
+    if (tokens == 0) return hipSuccess;
+    hipLaunchKernelGGL((append_kernel<DT, D>), dim3((tokens + kWavesPerGroup - 1) / kWavesPerGroup),
+                       dim3(64 * kWavesPerGroup), 0, stream, a, p);
     return hipGetLastError();
   }
 };
@@ -439,15 +773,46 @@ template <int DT, int D>
 struct PrefillL {
   static hipError_t run(const AttnArgs& a, const PrefillPlan& p, int n_tiles, hipStream_t stream) {
     if (n_tiles == 0) return hipSuccess;
-    hipLaunchKernelGGL((prefill_kernel<DT, D>), dim3(n_tiles, a.hkv), dim3(64 * kWavesPerGroup), 0, stream, a, p);
+    if (DT == 0) {
+      hipLaunchKernelGGL((prefill_mfma_kernel<D>), dim3((unsigned)n_tiles * a.hkv), dim3(256), 0, stream, a, p);
+    } else {
+      hipLaunchKernelGGL((prefill_kernel<DT, D>), dim3(n_tiles, a.hkv), dim3(64 * kWavesPerGroup), 0, stream, a, p);
+    }
     return hipGetLastError();
   }
 };
 
 }  // namespace
 
-hipError_t launch_append(const AppendArgs& a, int dtype, int head_dim, hipStream_t stream) {
-  return dispatch<AppendL>(dtype, head_dim, a, stream);
+hipError_t launch_append(const AppendArgs& a, const AppendPlan& p, int dtype, int head_dim, hipStream_t stream) {
+  return dispatch<AppendL>(dtype, head_dim, a, p, stream);
+}
+
+int decode_wave_slots(int dtype, int head_dim) {
+  // Concurrent decode waves the device can hold: workgroups per CU at this
+  // kernel's register use, times waves per workgroup, times CUs.  Cached per
+  // device; 2048 when there is no device to ask.
+  static std::atomic<int> cache[64][2][2];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 2048;
+  const int di = dtype == 0 ? 0 : 1, hi = head_dim == 128 ? 0 : 1;
+  const int known = cache[dev][di][hi].load(std::memory_order_relaxed);
+  if (known > 0) return known;
+  int cus = 0, per_cu = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) return 2048;
+  hipError_t e = hipErrorInvalidValue;
+  if (dtype == 0 && head_dim == 128)
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_kernel<0, 128>, 256, 0);
+  else if (dtype == 0 && head_dim == 64)
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_kernel<0, 64>, 256, 0);
+  else if (dtype == 1 && head_dim == 128)
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_kernel<1, 128>, 256, 0);
+  else if (dtype == 1 && head_dim == 64)
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_kernel<1, 64>, 256, 0);
+  if (e != hipSuccess || per_cu <= 0) return 2048;
+  const int slots = per_cu * kWavesPerGroup * cus;
+  cache[dev][di][hi].store(slots, std::memory_order_relaxed);
+  return slots;
 }
 hipError_t launch_decode(const AttnArgs& a, const DecodePlan& p, int n_items, int dtype, int head_dim,
                          hipStream_t stream) {

@@ -200,6 +200,30 @@ def test_mixed_equals_parts(torch_gpu):
         assert torch.equal(l, l_all.index_select(0, rows))
 
 
+def test_phases_equal_mixed_call(torch_gpu):
+    """mpa_decode_attention then mpa_prefill_attention (here on two streams)
+    give the mixed call's bits."""
+    import torch
+
+    rng = np.random.default_rng(30)
+    b = make_batch(mixed_specs(rng), HeadSpec(32, 8, 128), "bf16", rng)
+    d = to_device(b)
+    o_all, l_all = run_step(d)
+    out = torch.full_like(d.q, float("nan"))
+    lse = torch.full(d.q.shape[:2], float("nan"), dtype=torch.float32, device="cuda")
+    ws = mpa.alloc_workspace(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.qsl_host, d.scale)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    mpa.decode_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
+                         d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws, scale=d.scale, stream=s1)
+    mpa.prefill_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
+                          d.seq_lens_host, d.qsl_host, out, lse=lse, scale=d.scale, stream=s2)
+    torch.cuda.synchronize()
+    rows = torch.from_numpy(np.repeat(b.q_lens > 0, b.q_lens)).cuda()
+    assert torch.equal(out[rows].view(torch.int16), o_all[rows].view(torch.int16))
+    assert torch.equal(lse[rows], l_all[rows])
+
+
 def test_run_to_run_deterministic(torch_gpu):
     import torch
 

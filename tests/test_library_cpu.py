@@ -71,6 +71,8 @@ def append_rc(sh, seq_lens, qsl, bt=None):
     (dict(dtype=7), mpa.MPA_ERR_UNSUPPORTED),
     (dict(num_kv_heads=0), mpa.MPA_ERR_INVALID),
     (dict(scale=float("nan")), mpa.MPA_ERR_INVALID),
+    (dict(scale=0.0), mpa.MPA_ERR_INVALID),
+    (dict(scale=-0.1), mpa.MPA_ERR_INVALID),
 ])
 def test_unsupported_shapes_rejected(kw, code):
     sh = shape(**kw)
@@ -145,6 +147,9 @@ def test_plan_info_counts():
     qsl = [0, 1, 2, 72, 72, 74]
     info = mpa.plan_info(sh, seq_lens, qsl)
     assert info.num_decode_seqs == 2 and info.num_prefill_seqs == 2
-    # 64 (token, head) rows per tile: G = 4 -> 16 tokens per tile
-    assert info.num_prefill_tiles == (-(-70 // 16) + 1) * 2
+    # bf16 tiles hold 128 (token, head) rows: G = 4 -> 32 tokens per tile
+    assert info.num_prefill_tiles == (-(-70 // 32) + 1) * 2
+    # f32 tiles hold 64 rows: 16 tokens per tile
+    sh32 = shape(num_seqs=5, total_q_tokens=74, max_blocks_per_seq=64, dtype=mpa.MPA_F32)
+    assert mpa.plan_info(sh32, seq_lens, qsl).num_prefill_tiles == (-(-70 // 16) + 1) * 2
     assert info.decode_launches == 1
