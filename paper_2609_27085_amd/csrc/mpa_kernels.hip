@@ -45,6 +45,12 @@ __device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __device__ inline short bf16_bits(float x) { return __builtin_bit_cast(short, (__bf16)x); }
 
+// 16 bytes per lane from global memory straight into LDS: lane l's bytes land
+// at lds + 16*l (lds must be the same for the whole wave).
+__device__ inline void global_to_lds16(const void* g, void* lds) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+
 // ---------------------------------------------------------------------------
 // Element-type traits.  A "round" of the QK^T product consumes one 16-byte
 // chunk of K and of Q per lane: one 16x16x32 bf16 MFMA, or four 16x16x4 f32
@@ -459,13 +465,15 @@ __global__ __launch_bounds__(256) void prefill_kernel(AttnArgs a, PrefillPlan p)
 // and head r % G of the group, so the G heads that share a KV head share
 // every K/V tile.  Each wave owns 32 rows (one 32-wide MFMA column tile).
 //
-// Per 64-key tile (4 cache blocks), staged in LDS and double-buffered:
+// Per 64-key tile (4 cache blocks), double-buffered in LDS:
 //   S^T[64 keys][32 rows] = K . Q^T   2 x (D/16) v_mfma_f32_32x32x16_bf16
 //   O^T[D][32 rows]     += V^T . P^T  (D/32) x 4 v_mfma_f32_32x32x16_bf16
-// K is copied to LDS verbatim (a block is [D/8 chunks][16 keys][8]); each
-// 16-key row of V^T is copied with its 4-key groups 1 and 2 swapped, so that
-// the 8 keys one lane feeds the PV product (keys 4h..4h+3 and 8+4h..8+4h+3 of
-// a block, from the 32x32 output layout of S^T) are 16 contiguous bytes.
+// Both tiles are verbatim copies of the cache granules, fetched straight
+// into LDS (global_load_lds, 16 bytes a lane), so no registers stage them.
+// Row m of a 32-key S^T tile is key 16(m/16) + swap23(m%16), where swap23
+// exchanges bits 2 and 3: then the 8 keys a lane holds for one 16-key PV step
+// (output rows 8j+4h+i, j in {2t', 2t'+1}) are keys 8h..8h+7 of the block, one
+// contiguous 16-byte run of each V^T row.
 //
 // Softmax: exact online softmax with a lazily updated reference maximum.  The
 // running reference m only moves when a row's new maximum exceeds it by more
@@ -479,9 +487,10 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(AttnArgs a, Prefil
   constexpr int BLK = kBlock * D;        // elements of one (block, head) granule
   constexpr int KS = D / 16;             // k-steps of the QK^T product
   constexpr int DT = D / 32;             // 32-dim row tiles of O^T
-  constexpr int KCH = NB * BLK / 8 / 256;  // 16-byte K chunks each thread copies
-  constexpr int VR = NB * D / 256;         // 32-byte V^T rows each thread copies
-  static_assert(KCH >= 1 && VR >= 1, "tile copy shape");
+  constexpr int NI = NB * BLK * 2 / 1024;  // 1 KB wave copies per tile and cache
+  constexpr int WI = NI / 4;               // ... per wave
+  constexpr int VR = NB * D / 256;         // V^T rows each thread fixes up in a tail tile
+  static_assert(WI >= 1 && VR >= 1, "tile copy shape");
   __shared__ __attribute__((aligned(16))) uint16_t sk[2][NB * BLK];
   __shared__ __attribute__((aligned(16))) uint16_t sv[2][NB * BLK];
 
@@ -526,74 +535,49 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(AttnArgs a, Prefil
       qf[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(q + (2 * ks + h) * 8));
   }
 
-  // ---- global -> registers -> LDS tile copy
-  u32x4 kreg[KCH];
-  u32x4 vreg[VR][2];
-  auto load_tile = [&](int kt) {
+  // ---- global -> LDS tile copy
+  // Block ids of a tile are fetched one tile ahead by lanes 0..NB-1 and
+  // broadcast with readlane.  A block index past the sequence's last needed
+  // block is clamped to it (its keys are all masked, and its V rows are
+  // zeroed in the fix-up below), so every copy is unconditional.
+  const int nblk = (kend + kBlock - 1) / kBlock;
+  auto tile_ids = [&](int kt) -> int { return lane < NB ? bt[min(kt * NB + lane, nblk - 1)] : 0; };
+  auto copy_tile = [&](int buf, int ids) {
 #pragma unroll
-    for (int u = 0; u < KCH; ++u) {
-      const int ci = tid + 256 * u;
-      const int bi = ci / (BLK / 8);
-      const int kb = kt * NB + bi;
-      u32x4 val = {0u, 0u, 0u, 0u};
-      if (kb * kBlock < kend) {
-        int blk = bt[kb];
-        if (blk >= 0 && blk < a.nb)
-          val = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(a.k_cache) +
-                                                ((size_t)blk * a.hkv + g) * BLK + (ci % (BLK / 8)) * 8);
-      }
-      kreg[u] = val;
+    for (int u = 0; u < WI; ++u) {
+      const int ii = wave * WI + u;         // this wave's 1 KB slice of the tile
+      const int bi = (ii * 512) / BLK;      // block within the tile (wave-uniform)
+      const int off = (ii * 512) % BLK + lane * 8;
+      int blk = __builtin_amdgcn_readlane(ids, bi);
+      blk = (blk >= 0 && blk < a.nb) ? blk : 0;
+      const size_t gbase = ((size_t)blk * a.hkv + g) * BLK + off;
+      global_to_lds16(reinterpret_cast<const uint16_t*>(a.k_cache) + gbase, &sk[buf][ii * 512]);
+      global_to_lds16(reinterpret_cast<const uint16_t*>(a.v_cache) + gbase, &sv[buf][ii * 512]);
     }
+  };
+  // Keys >= L of the tile (the tail of the sequence's last block, and clamped
+  // blocks) may hold NaN/Inf: zero their V^T entries; a block with an invalid
+  // id gets NaN values instead, poisoning the rows that read it.  Runs only
+  // for the (rare) tiles that need it, between two barriers.
+  auto fix_tile = [&](int buf, int kt, int ids) {
 #pragma unroll
     for (int u = 0; u < VR; ++u) {
       const int ri = tid + 256 * u;
       const int bi = ri / D;
-      const int d = ri % D;
-      const int kb = kt * NB + bi;
-      u32x4 lo = {0u, 0u, 0u, 0u}, hi = {0u, 0u, 0u, 0u};
-      if (kb * kBlock < kend) {
-        int blk = bt[kb];
-        if (blk >= 0 && blk < a.nb) {
-          const uint16_t* src =
-              reinterpret_cast<const uint16_t*>(a.v_cache) + ((size_t)blk * a.hkv + g) * BLK + d * kBlock;
-          lo = *reinterpret_cast<const u32x4*>(src);
-          hi = *reinterpret_cast<const u32x4*>(src + 8);
-          // keys >= L of the sequence's last block may hold NaN/Inf: zero them
-          const int nvalid = L - kb * kBlock;
-          if (nvalid < kBlock) {
+      const int blk = __shfl(ids, bi);
+      uint16_t* rowp = &sv[buf][ri * kBlock];
+      if (!(blk >= 0 && blk < a.nb)) {
 #pragma unroll
-            for (int w = 0; w < 8; ++w) {
-              const int k0 = 2 * w;
-              unsigned int word = w < 4 ? lo[w] : hi[w - 4];
-              word = k0 >= nvalid ? 0u : (k0 + 1 >= nvalid ? (word & 0xFFFFu) : word);
-              if (w < 4) lo[w] = word; else hi[w - 4] = word;
-            }
-          }
-        } else {
-          const u32x4 nan2 = {0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u};
-          lo = nan2;  // an invalid block id poisons the rows that read this tile
-          hi = nan2;
-        }
+        for (int e = 0; e < kBlock; ++e) rowp[e] = 0x7FC0;
+      } else {
+        const int nvalid = L - (kt * NB + bi) * kBlock;
+        for (int e = max(nvalid, 0); e < kBlock; ++e) rowp[e] = 0;
       }
-      vreg[u][0] = lo;
-      vreg[u][1] = hi;
     }
   };
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < KCH; ++u) {
-      const int ci = tid + 256 * u;
-      *reinterpret_cast<u32x4*>(&sk[buf][ci * 8]) = kreg[u];
-    }
-#pragma unroll
-    for (int u = 0; u < VR; ++u) {
-      const int ri = tid + 256 * u;
-      const u32x4 lo = vreg[u][0], hi = vreg[u][1];
-      const u32x4 a0 = {lo[0], lo[1], hi[0], hi[1]};  // keys 0-3, 8-11
-      const u32x4 a1 = {lo[2], lo[3], hi[2], hi[3]};  // keys 4-7, 12-15
-      *reinterpret_cast<u32x4*>(&sv[buf][ri * kBlock]) = a0;
-      *reinterpret_cast<u32x4*>(&sv[buf][ri * kBlock + 8]) = a1;
-    }
+  auto tile_needs_fix = [&](int kt, int ids) {
+    const int blk = lane < NB ? ids : 0;
+    return kt * BN + BN > L || __any(!(blk >= 0 && blk < a.nb));
   };
 
   f32x16 o[DT];
@@ -605,35 +589,51 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(AttnArgs a, Prefil
   const float thresh = 8.f / c;  // 8 in log2 units, in raw score units
   float m_ref = -INFINITY;       // reference maximum, raw score units
   float l = 0.f;
+  // K operand row of this lane: key swap23(n%16) of block n/16 of a 32-key tile
+  const int kk = n & 15;
+  const int koff = (n >> 4) * BLK + ((kk & 3) | ((kk & 4) << 1) | ((kk & 8) >> 1)) * 8;
 
-  load_tile(0);
-  store_tile(0);
+  int ids_cur = tile_ids(0);
+  copy_tile(0, ids_cur);
+  int ids_next = tile_ids(1);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
+  if (tile_needs_fix(0, ids_cur)) {
+    fix_tile(0, 0, ids_cur);
+    __syncthreads();
+  }
   for (int kt = 0; kt < ntile; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < ntile) load_tile(kt + 1);
+    const bool more = kt + 1 < ntile;
+    if (more) copy_tile(buf ^ 1, ids_next);
+    const int ids_this_next = ids_next;
+    ids_next = tile_ids(kt + 2);
     const int key_base = kt * BN;
     if (wave_active && key_base < w_kend) {
       const uint16_t* K = sk[buf];
       const uint16_t* V = sv[buf];
       f32x16 st[2];
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
+      for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) st[rt][r] = 0.f;
-        const uint16_t* kbase = K + (2 * rt + (n >> 4)) * BLK + (n & 15) * 8;
+      // the two 32-key row tiles are independent accumulation chains:
+      // interleave them so back-to-back MFMAs never wait on each other
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
+      for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt) {
+          const uint16_t* kbase = K + (2 * rt) * BLK + koff;
           const bf16x8 kf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kbase + (2 * ks + h) * 128));
           st[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], st[rt], 0, 0, 0);
         }
-      }
       if (key_base + BN - 1 > w_min_limit) {
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int key = key_base + 32 * rt + 8 * (r >> 2) + 4 * h + (r & 3);
+            const int jr = r >> 2;
+            const int key = key_base + 32 * rt + 16 * (jr >> 1) + 8 * h + 4 * (jr & 1) + (r & 3);
             if (key > limit) st[rt][r] = -INFINITY;
           }
       }
@@ -672,8 +672,12 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(AttnArgs a, Prefil
         }
       }
     }
-    if (kt + 1 < ntile) store_tile(buf ^ 1);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+    if (more && tile_needs_fix(kt + 1, ids_this_next)) {
+      fix_tile(buf ^ 1, kt + 1, ids_this_next);
+      __syncthreads();
+    }
   }
 
   const float lt = l + __shfl_xor(l, 32);
