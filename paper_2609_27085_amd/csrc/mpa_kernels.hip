@@ -46,9 +46,14 @@ __device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ inline short bf16_bits(float x) { return __builtin_bit_cast(short, (__bf16)x); }
 
 // 16 bytes per lane from global memory straight into LDS: lane l's bytes land
-// at lds + 16*l (lds must be the same for the whole wave).
+// at lds + 16*l (lds must be the same for the whole wave).  Issued as inline
+// assembly so that the compiler does not make every later LDS read wait for
+// it (it cannot tell that the read targets the other buffer); the caller
+// waits with an explicit "s_waitcnt vmcnt(0)" before the barrier that
+// publishes the tile.  M0 is written only here in this file.
 __device__ inline void global_to_lds16(const void* g, void* lds) {
-  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+  const unsigned off = (unsigned)(size_t)(__attribute__((address_space(3))) void*)lds;
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(off) : "memory");
 }
 
 // ---------------------------------------------------------------------------
@@ -468,12 +473,17 @@ __global__ __launch_bounds__(256) void prefill_kernel(AttnArgs a, PrefillPlan p)
 // Per 64-key tile (4 cache blocks), double-buffered in LDS:
 //   S^T[64 keys][32 rows] = K . Q^T   2 x (D/16) v_mfma_f32_32x32x16_bf16
 //   O^T[D][32 rows]     += V^T . P^T  (D/32) x 4 v_mfma_f32_32x32x16_bf16
-// Both tiles are verbatim copies of the cache granules, fetched straight
-// into LDS (global_load_lds, 16 bytes a lane), so no registers stage them.
-// Row m of a 32-key S^T tile is key 16(m/16) + swap23(m%16), where swap23
-// exchanges bits 2 and 3: then the 8 keys a lane holds for one 16-key PV step
-// (output rows 8j+4h+i, j in {2t', 2t'+1}) are keys 8h..8h+7 of the block, one
-// contiguous 16-byte run of each V^T row.
+// Both tiles are fetched straight into LDS (global_load_lds, 16 bytes a lane),
+// so no registers stage them; the per-lane source addresses permute 16-byte
+// pieces so that every MFMA operand read from LDS is one contiguous run per
+// 16 lanes (no bank conflicts):
+//  * row m of a 32-key S^T tile is key 16(m/16) + swap23(m%16), where swap23
+//    exchanges bits 2 and 3.  Then the 8 keys a lane holds for one 16-key PV
+//    step (output rows 8j+4h+i, j in {2t', 2t'+1}) are keys 8h..8h+7 of the
+//    block.  LDS holds each K chunk row with its 16 slots already in that
+//    order: [block][d/8 chunks][slot][8], slot s = key swap23(s);
+//  * LDS holds V^T as [block][key half h][d][8 keys], so lane (m, h) of a PV
+//    step reads row 32dt+m of half h.
 //
 // Softmax: exact online softmax with a lazily updated reference maximum.  The
 // running reference m only moves when a row's new maximum exceeds it by more
@@ -489,7 +499,7 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(AttnArgs a, Prefil
   constexpr int DT = D / 32;             // 32-dim row tiles of O^T
   constexpr int NI = NB * BLK * 2 / 1024;  // 1 KB wave copies per tile and cache
   constexpr int WI = NI / 4;               // ... per wave
-  constexpr int VR = NB * D / 256;         // V^T rows each thread fixes up in a tail tile
+  constexpr int VR = NB * 2 * D / 256;     // 8-key V^T pieces each thread fixes up in a tail tile
   static_assert(WI >= 1 && VR >= 1, "tile copy shape");
   __shared__ __attribute__((aligned(16))) uint16_t sk[2][NB * BLK];
   __shared__ __attribute__((aligned(16))) uint16_t sv[2][NB * BLK];
@@ -545,14 +555,19 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(AttnArgs a, Prefil
   auto copy_tile = [&](int buf, int ids) {
 #pragma unroll
     for (int u = 0; u < WI; ++u) {
-      const int ii = wave * WI + u;         // this wave's 1 KB slice of the tile
-      const int bi = (ii * 512) / BLK;      // block within the tile (wave-uniform)
-      const int off = (ii * 512) % BLK + lane * 8;
+      const int ii = wave * WI + u;                 // this wave's 1 KB slice of the tile
+      const int bi = (ii * 64) / (BLK / 8);         // block within the tile (wave-uniform)
+      const int cq = (ii * 64) % (BLK / 8) + lane;  // 16-byte piece within the block
       int blk = __builtin_amdgcn_readlane(ids, bi);
       blk = (blk >= 0 && blk < a.nb) ? blk : 0;
-      const size_t gbase = ((size_t)blk * a.hkv + g) * BLK + off;
-      global_to_lds16(reinterpret_cast<const uint16_t*>(a.k_cache) + gbase, &sk[buf][ii * 512]);
-      global_to_lds16(reinterpret_cast<const uint16_t*>(a.v_cache) + gbase, &sv[buf][ii * 512]);
+      const size_t gran = ((size_t)blk * a.hkv + g) * BLK;
+      // K: piece (chunk c, slot) <- key swap23(slot) of chunk c
+      const int kc = cq >> 4, ks16 = cq & 15;
+      const int kkey = (ks16 & 3) | ((ks16 & 4) << 1) | ((ks16 & 8) >> 1);
+      global_to_lds16(reinterpret_cast<const uint16_t*>(a.k_cache) + gran + (kc * 16 + kkey) * 8, &sk[buf][ii * 512]);
+      // V: piece (half vh, row d) <- keys 8vh..8vh+7 of V^T row d
+      const int vh = cq / D, vd = cq % D;
+      global_to_lds16(reinterpret_cast<const uint16_t*>(a.v_cache) + gran + vd * kBlock + vh * 8, &sv[buf][ii * 512]);
     }
   };
   // Keys >= L of the tile (the tail of the sequence's last block, and clamped
@@ -562,16 +577,17 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(AttnArgs a, Prefil
   auto fix_tile = [&](int buf, int kt, int ids) {
 #pragma unroll
     for (int u = 0; u < VR; ++u) {
-      const int ri = tid + 256 * u;
-      const int bi = ri / D;
+      const int ri = tid + 256 * u;  // (block, half, row) piece of 8 keys
+      const int bi = ri / (2 * D);
+      const int vh = (ri / D) & 1;
       const int blk = __shfl(ids, bi);
-      uint16_t* rowp = &sv[buf][ri * kBlock];
+      uint16_t* piece = &sv[buf][ri * 8];
       if (!(blk >= 0 && blk < a.nb)) {
 #pragma unroll
-        for (int e = 0; e < kBlock; ++e) rowp[e] = 0x7FC0;
+        for (int e = 0; e < 8; ++e) piece[e] = 0x7FC0;
       } else {
-        const int nvalid = L - (kt * NB + bi) * kBlock;
-        for (int e = max(nvalid, 0); e < kBlock; ++e) rowp[e] = 0;
+        const int nvalid = L - (kt * NB + bi) * kBlock - 8 * vh;  // valid keys of this piece
+        for (int e = max(nvalid, 0); e < 8; ++e) piece[e] = 0;
       }
     }
   };
@@ -589,9 +605,8 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(AttnArgs a, Prefil
   const float thresh = 8.f / c;  // 8 in log2 units, in raw score units
   float m_ref = -INFINITY;       // reference maximum, raw score units
   float l = 0.f;
-  // K operand row of this lane: key swap23(n%16) of block n/16 of a 32-key tile
-  const int kk = n & 15;
-  const int koff = (n >> 4) * BLK + ((kk & 3) | ((kk & 4) << 1) | ((kk & 8) >> 1)) * 8;
+  // K operand row of this lane: slot n%16 of block n/16 of a 32-key tile
+  const int koff = (n >> 4) * BLK + (n & 15) * 8;
 
   int ids_cur = tile_ids(0);
   copy_tile(0, ids_cur);
@@ -664,10 +679,10 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(AttnArgs a, Prefil
       }
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        const uint16_t* vbase = V + t * BLK + n * kBlock + 8 * h;
+        const uint16_t* vbase = V + t * BLK + (h * D + n) * 8;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-          const bf16x8 vf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(vbase + 32 * dt * kBlock));
+          const bf16x8 vf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(vbase + 32 * dt * 8));
           o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[t], o[dt], 0, 0, 0);
         }
       }
