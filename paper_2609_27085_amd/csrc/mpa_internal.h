@@ -12,7 +12,7 @@ constexpr int kBlock = 16;            // tokens per cache block
 constexpr int kWavesPerGroup = 4;     // waves per workgroup in every kernel
 constexpr int kMaxPlanSeqs = 256;     // sequences per launch (kernel-argument plan)
 constexpr int kPrefillRows = 64;      // (token, head) rows per f32 prefill workgroup
-constexpr int kPrefillRowsMfma = 128; // (token, head) rows per bf16 prefill workgroup
+constexpr int kPrefillRowsMfma = 256; // (token, head) rows per bf16 prefill workgroup (8 waves)
 
 // Pointers and sizes common to the attention kernels.
 struct AttnArgs {

@@ -48,9 +48,19 @@ __device__ inline short bf16_bits(float x) { return __builtin_bit_cast(short, (_
 // 16 bytes per lane from global memory straight into LDS: lane l's bytes land
 // at lds + 16*l (lds must be the same for the whole wave).  Issued as inline
 // assembly so that the compiler does not make every later LDS read wait for
-// it (it cannot tell that the read targets the other buffer); the caller
-// waits with an explicit "s_waitcnt vmcnt(0)" before the barrier that
-// publishes the tile.  M0 is written only here in this file.
+// it (it cannot tell that the read targets another buffer); the caller waits
+// with an explicit vector-memory wait before the barrier that publishes the
+// tile.  M0 is written only here in this file.
+// s_waitcnt immediate that waits until at most n vector-memory operations are
+// outstanding (expcnt and lgkmcnt left at their maxima).  Used through the
+// intrinsic, which the compiler's own wait-count tracking understands.
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+#define MPA_WAIT_VMCNT(n)                          \
+  do {                                             \
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(n));      \
+    asm volatile("" ::: "memory");                 \
+  } while (0)
+
 __device__ inline void global_to_lds16(const void* g, void* lds) {
   const unsigned off = (unsigned)(size_t)(__attribute__((address_space(3))) void*)lds;
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(off) : "memory");
@@ -465,18 +475,19 @@ __global__ __launch_bounds__(256) void prefill_kernel(AttnArgs a, PrefillPlan p)
 }
 
 // ---------------------------------------------------------------------------
-// Prefill chunks, bf16: the tensor-core path.  One workgroup of 4 waves per
-// (sequence, 128-row query tile, KV head); row r of the tile is token r / G
-// and head r % G of the group, so the G heads that share a KV head share
+// Prefill chunks, bf16: the tensor-core path.  One workgroup of WAVES waves
+// per (sequence, 32*WAVES-row query tile, KV head); row r of the tile is token
+// r / G and head r % G of the group, so the G heads that share a KV head share
 // every K/V tile.  Each wave owns 32 rows (one 32-wide MFMA column tile).
 //
-// Per 64-key tile (4 cache blocks), double-buffered in LDS:
+// Per 64-key tile (4 cache blocks), in a STAGES-deep LDS ring:
 //   S^T[64 keys][32 rows] = K . Q^T   2 x (D/16) v_mfma_f32_32x32x16_bf16
 //   O^T[D][32 rows]     += V^T . P^T  (D/32) x 4 v_mfma_f32_32x32x16_bf16
-// Both tiles are fetched straight into LDS (global_load_lds, 16 bytes a lane),
-// so no registers stage them; the per-lane source addresses permute 16-byte
-// pieces so that every MFMA operand read from LDS is one contiguous run per
-// 16 lanes (no bank conflicts):
+// Tiles are fetched straight into LDS (global_load_lds, 16 bytes a lane) by
+// the waves themselves, STAGES-1 tiles ahead of use, so no registers stage
+// them and a copy has STAGES-1 tiles of compute to land in.  The per-lane
+// source addresses permute 16-byte pieces so that every MFMA operand read
+// from LDS is one contiguous run per 16 lanes (no bank conflicts):
 //  * row m of a 32-key S^T tile is key 16(m/16) + swap23(m%16), where swap23
 //    exchanges bits 2 and 3.  Then the 8 keys a lane holds for one 16-key PV
 //    step (output rows 8j+4h+i, j in {2t', 2t'+1}) are keys 8h..8h+7 of the
@@ -484,29 +495,35 @@ __global__ __launch_bounds__(256) void prefill_kernel(AttnArgs a, PrefillPlan p)
 //    order: [block][d/8 chunks][slot][8], slot s = key swap23(s);
 //  * LDS holds V^T as [block][key half h][d][8 keys], so lane (m, h) of a PV
 //    step reads row 32dt+m of half h.
+// Each wave copies whole blocks of a tile, so it reads one block id per tile
+// (a scalar load) and fixes up its own pieces (zeroing V entries of keys >= L,
+// which may hold NaN/Inf; NaN for an invalid block id) before the barrier
+// that publishes the tile.
 //
 // Softmax: exact online softmax with a lazily updated reference maximum.  The
 // running reference m only moves when a row's new maximum exceeds it by more
 // than 8 (log2 units), so exp2(s - m) <= 2^8 and the O / l rescale is skipped
 // for almost every tile; the final O / l is the same quotient either way.
-template <int D>
-__global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(AttnArgs a, PrefillPlan p) {
+template <int D, int WAVES, int STAGES>
+__global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a, PrefillPlan p) {
   using f32x16 = float __attribute__((ext_vector_type(16)));
-  constexpr int BN = 64;                 // keys per tile
-  constexpr int NB = BN / kBlock;        // cache blocks per tile
-  constexpr int BLK = kBlock * D;        // elements of one (block, head) granule
-  constexpr int KS = D / 16;             // k-steps of the QK^T product
-  constexpr int DT = D / 32;             // 32-dim row tiles of O^T
-  constexpr int NI = NB * BLK * 2 / 1024;  // 1 KB wave copies per tile and cache
-  constexpr int WI = NI / 4;               // ... per wave
-  constexpr int VR = NB * 2 * D / 256;     // 8-key V^T pieces each thread fixes up in a tail tile
-  static_assert(WI >= 1 && VR >= 1, "tile copy shape");
-  __shared__ __attribute__((aligned(16))) uint16_t sk[2][NB * BLK];
-  __shared__ __attribute__((aligned(16))) uint16_t sv[2][NB * BLK];
+  using cint = const __attribute__((address_space(4))) int32_t;
+  constexpr int BN = 64;                   // keys per tile
+  constexpr int NB = BN / kBlock;          // cache blocks per tile
+  constexpr int BLK = kBlock * D;          // elements of one (block, head) granule
+  constexpr int TILE = NB * BLK;           // elements of one K (or V) tile
+  constexpr int KS = D / 16;               // k-steps of the QK^T product
+  constexpr int DT = D / 32;               // 32-dim row tiles of O^T
+  constexpr int NI = TILE * 2 / 1024;      // 1 KB copies per tile and cache
+  constexpr int WI = NI / WAVES;           // ... per wave
+  static_assert(WI >= 1 && NI % WAVES == 0 && (WI * 512) <= BLK && BLK % (WI * 512) == 0,
+                "each wave copies part of exactly one block per tile");
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+  uint16_t* const sk = smem;                   // STAGES K tiles
+  uint16_t* const sv = smem + STAGES * TILE;   // STAGES V tiles
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = wave_uniform(tid >> 6);
+  const int lane = threadIdx.x & 63;
+  const int wave = wave_uniform(threadIdx.x >> 6);
   const int n_tiles = p.tile_start[p.n_seqs];
   const int g = blockIdx.x % a.hkv;
   const int tile = n_tiles - 1 - (int)(blockIdx.x / a.hkv);  // last (longest) query tiles first
@@ -522,7 +539,7 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(AttnArgs a, Prefil
   const int last_tok = min(first_tok + p.q_tile - 1, C - 1);
   const int kend = P + last_tok + 1;  // keys the workgroup needs
   const int ntile = (kend + BN - 1) / BN;
-  const int32_t* bt = a.block_tables + (size_t)s * a.mb;
+  cint* bt = (cint*)(a.block_tables + (size_t)s * a.mb);
 
   // this lane's query row
   const int n = lane & 31, h = lane >> 5;
@@ -545,55 +562,52 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(AttnArgs a, Prefil
       qf[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(q + (2 * ks + h) * 8));
   }
 
-  // ---- global -> LDS tile copy
-  // Block ids of a tile are fetched one tile ahead by lanes 0..NB-1 and
-  // broadcast with readlane.  A block index past the sequence's last needed
-  // block is clamped to it (its keys are all masked, and its V rows are
-  // zeroed in the fix-up below), so every copy is unconditional.
+  // ---- global -> LDS tile copies (this wave's slices)
   const int nblk = (kend + kBlock - 1) / kBlock;
-  auto tile_ids = [&](int kt) -> int { return lane < NB ? bt[min(kt * NB + lane, nblk - 1)] : 0; };
-  auto copy_tile = [&](int buf, int ids) {
+  const int my_bi = (wave * WI * 512) / BLK;  // the tile block this wave copies
+  // Tile kt's copy.  A block index past the sequence's last needed block is
+  // clamped to it (its keys are all masked and its V entries zeroed), so
+  // every copy is issued, always 2*WI instructions per wave per tile.
+  auto copy_tile = [&](int kt) -> int {
+    const int stage = kt % STAGES;
+    const int blk_raw = bt[min(kt * NB + my_bi, nblk - 1)];
+    const int blk = (blk_raw >= 0 && blk_raw < a.nb) ? blk_raw : 0;
+    const size_t gran = ((size_t)blk * a.hkv + g) * BLK;
 #pragma unroll
     for (int u = 0; u < WI; ++u) {
-      const int ii = wave * WI + u;                 // this wave's 1 KB slice of the tile
-      const int bi = (ii * 64) / (BLK / 8);         // block within the tile (wave-uniform)
+      const int ii = wave * WI + u;                 // 1 KB slice of the tile
       const int cq = (ii * 64) % (BLK / 8) + lane;  // 16-byte piece within the block
-      int blk = __builtin_amdgcn_readlane(ids, bi);
-      blk = (blk >= 0 && blk < a.nb) ? blk : 0;
-      const size_t gran = ((size_t)blk * a.hkv + g) * BLK;
       // K: piece (chunk c, slot) <- key swap23(slot) of chunk c
       const int kc = cq >> 4, ks16 = cq & 15;
       const int kkey = (ks16 & 3) | ((ks16 & 4) << 1) | ((ks16 & 8) >> 1);
-      global_to_lds16(reinterpret_cast<const uint16_t*>(a.k_cache) + gran + (kc * 16 + kkey) * 8, &sk[buf][ii * 512]);
+      global_to_lds16(reinterpret_cast<const uint16_t*>(a.k_cache) + gran + (kc * 16 + kkey) * 8,
+                      sk + stage * TILE + ii * 512);
       // V: piece (half vh, row d) <- keys 8vh..8vh+7 of V^T row d
       const int vh = cq / D, vd = cq % D;
-      global_to_lds16(reinterpret_cast<const uint16_t*>(a.v_cache) + gran + vd * kBlock + vh * 8, &sv[buf][ii * 512]);
+      global_to_lds16(reinterpret_cast<const uint16_t*>(a.v_cache) + gran + vd * kBlock + vh * 8,
+                      sv + stage * TILE + ii * 512);
     }
+    return blk_raw;
   };
-  // Keys >= L of the tile (the tail of the sequence's last block, and clamped
-  // blocks) may hold NaN/Inf: zero their V^T entries; a block with an invalid
-  // id gets NaN values instead, poisoning the rows that read it.  Runs only
-  // for the (rare) tiles that need it, between two barriers.
-  auto fix_tile = [&](int buf, int kt, int ids) {
+  // After this wave's copy of tile kt has landed: zero its V entries of keys
+  // >= L (the tail of the sequence's last block, and clamped blocks), or fill
+  // them with NaN when the block id was invalid.
+  auto fix_tile = [&](int kt, int blk_raw) {
+    const int nvalid_blk = L - (kt * NB + my_bi) * kBlock;
+    const bool bad = !(blk_raw >= 0 && blk_raw < a.nb);
+    if (!bad && nvalid_blk >= kBlock) return;
+    const int stage = kt % STAGES;
 #pragma unroll
-    for (int u = 0; u < VR; ++u) {
-      const int ri = tid + 256 * u;  // (block, half, row) piece of 8 keys
-      const int bi = ri / (2 * D);
-      const int vh = (ri / D) & 1;
-      const int blk = __shfl(ids, bi);
-      uint16_t* piece = &sv[buf][ri * 8];
-      if (!(blk >= 0 && blk < a.nb)) {
+    for (int u = 0; u < WI; ++u) {
+      const int ii = wave * WI + u;
+      const int cq = (ii * 64) % (BLK / 8) + lane;
+      const int vh = cq / D;
+      uint16_t* piece = sv + stage * TILE + ii * 512 + lane * 8;
+      const int nvalid = nvalid_blk - 8 * vh;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) piece[e] = 0x7FC0;
-      } else {
-        const int nvalid = L - (kt * NB + bi) * kBlock - 8 * vh;  // valid keys of this piece
-        for (int e = max(nvalid, 0); e < 8; ++e) piece[e] = 0;
-      }
+      for (int e = 0; e < 8; ++e)
+        if (bad || e >= nvalid) piece[e] = bad ? (uint16_t)0x7FC0 : (uint16_t)0;
     }
-  };
-  auto tile_needs_fix = [&](int kt, int ids) {
-    const int blk = lane < NB ? ids : 0;
-    return kt * BN + BN > L || __any(!(blk >= 0 && blk < a.nb));
   };
 
   f32x16 o[DT];
@@ -608,25 +622,24 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(AttnArgs a, Prefil
   // K operand row of this lane: slot n%16 of block n/16 of a 32-key tile
   const int koff = (n >> 4) * BLK + (n & 15) * 8;
 
-  int ids_cur = tile_ids(0);
-  copy_tile(0, ids_cur);
-  int ids_next = tile_ids(1);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  // the Q fragments (ordinary loads) land before any tile copy is issued, so
+  // that no wait inside the loop is ever needed for them
+  MPA_WAIT_VMCNT(0);
+  // prologue: tiles 0 .. STAGES-2 in flight; tile 0 published
+  int blk_id[STAGES];
+#pragma unroll
+  for (int k = 0; k < STAGES - 1; ++k) blk_id[k] = copy_tile(k);
+  MPA_WAIT_VMCNT(2 * WI * (STAGES - 2));
+  fix_tile(0, blk_id[0]);
   __syncthreads();
-  if (tile_needs_fix(0, ids_cur)) {
-    fix_tile(0, 0, ids_cur);
-    __syncthreads();
-  }
+
   for (int kt = 0; kt < ntile; ++kt) {
-    const int buf = kt & 1;
-    const bool more = kt + 1 < ntile;
-    if (more) copy_tile(buf ^ 1, ids_next);
-    const int ids_this_next = ids_next;
-    ids_next = tile_ids(kt + 2);
+    // copy tile kt+STAGES-1 into the stage tile kt-1 used (all waves are past it)
+    blk_id[(kt + STAGES - 1) % STAGES] = copy_tile(kt + STAGES - 1);
     const int key_base = kt * BN;
     if (wave_active && key_base < w_kend) {
-      const uint16_t* K = sk[buf];
-      const uint16_t* V = sv[buf];
+      const uint16_t* K = sk + (kt % STAGES) * TILE;
+      const uint16_t* V = sv + (kt % STAGES) * TILE;
       f32x16 st[2];
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt)
@@ -638,8 +651,8 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(AttnArgs a, Prefil
       for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
-          const uint16_t* kbase = K + (2 * rt) * BLK + koff;
-          const bf16x8 kf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kbase + (2 * ks + h) * 128));
+          const bf16x8 kf =
+              __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(K + 2 * rt * BLK + koff + (2 * ks + h) * 128));
           st[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], st[rt], 0, 0, 0);
         }
       if (key_base + BN - 1 > w_min_limit) {
@@ -687,13 +700,13 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(AttnArgs a, Prefil
         }
       }
     }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // this wave's part of tile kt+1 has landed once only the copies issued
+    // after it (tiles kt+2 .. kt+STAGES-1) remain in flight
+    MPA_WAIT_VMCNT(2 * WI * (STAGES - 2));
+    fix_tile(kt + 1, blk_id[(kt + 1) % STAGES]);
     __syncthreads();
-    if (more && tile_needs_fix(kt + 1, ids_this_next)) {
-      fix_tile(buf ^ 1, kt + 1, ids_this_next);
-      __syncthreads();
-    }
   }
+  MPA_WAIT_VMCNT(0);  // drain the clamped copies past the end
 
   const float lt = l + __shfl_xor(l, 32);
   if (!wave_active || !row_ok) return;
@@ -788,15 +801,35 @@ struct MergeL {
   }
 };
 
+constexpr int kPrefillWaves = 8;   // waves per bf16 prefill workgroup
+constexpr int kPrefillStages = 3;  // LDS ring depth of the bf16 prefill kernel
+
+template <int D>
+hipError_t launch_prefill_mfma(const AttnArgs& a, const PrefillPlan& p, int n_tiles, hipStream_t stream) {
+  constexpr size_t lds = 2 * kPrefillStages * 4 * kBlock * D * sizeof(uint16_t);
+  auto kern = prefill_mfma_kernel<D, kPrefillWaves, kPrefillStages>;
+  // The ring exceeds the default 64 KB of dynamic LDS; raise the limit once
+  // per device (each GPU keeps its own function attributes).
+  static std::atomic<unsigned long long> ready{0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return hipErrorInvalidDevice;
+  const unsigned long long bit = 1ull << (dev & 63);
+  if (!(ready.load(std::memory_order_relaxed) & bit)) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    ready.fetch_or(bit, std::memory_order_relaxed);
+  }
+  hipLaunchKernelGGL(kern, dim3((unsigned)n_tiles * a.hkv), dim3(64 * kPrefillWaves), lds, stream, a, p);
+  return hipGetLastError();
+}
+
 template <int DT, int D>
 struct PrefillL {
   static hipError_t run(const AttnArgs& a, const PrefillPlan& p, int n_tiles, hipStream_t stream) {
     if (n_tiles == 0) return hipSuccess;
-    if (DT == 0) {
-      hipLaunchKernelGGL((prefill_mfma_kernel<D>), dim3((unsigned)n_tiles * a.hkv), dim3(256), 0, stream, a, p);
-    } else {
-      hipLaunchKernelGGL((prefill_kernel<DT, D>), dim3(n_tiles, a.hkv), dim3(64 * kWavesPerGroup), 0, stream, a, p);
-    }
+    if (DT == 0) return launch_prefill_mfma<D>(a, p, n_tiles, stream);
+    hipLaunchKernelGGL((prefill_kernel<DT, D>), dim3(n_tiles, a.hkv), dim3(64 * kWavesPerGroup), 0, stream, a, p);
     return hipGetLastError();
   }
 };

@@ -147,8 +147,8 @@ def test_plan_info_counts():
     qsl = [0, 1, 2, 72, 72, 74]
     info = mpa.plan_info(sh, seq_lens, qsl)
     assert info.num_decode_seqs == 2 and info.num_prefill_seqs == 2
-    # bf16 tiles hold 128 (token, head) rows: G = 4 -> 32 tokens per tile
-    assert info.num_prefill_tiles == (-(-70 // 32) + 1) * 2
+    # bf16 tiles hold 256 (token, head) rows: G = 4 -> 64 tokens per tile
+    assert info.num_prefill_tiles == (-(-70 // 64) + 1) * 2
     # f32 tiles hold 64 rows: 16 tokens per tile
     sh32 = shape(num_seqs=5, total_q_tokens=74, max_blocks_per_seq=64, dtype=mpa.MPA_F32)
     assert mpa.plan_info(sh32, seq_lens, qsl).num_prefill_tiles == (-(-70 // 16) + 1) * 2
