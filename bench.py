@@ -179,6 +179,9 @@ def main(argv=None) -> int:
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--streams", type=int, default=1, choices=(1, 2),
+                    help="2: the decode and prefill halves of the step run concurrently on two streams "
+                         "(the library's mpa_decode_attention / mpa_prefill_attention); 1 (default): one after the other")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes 5 times (the reference kernel "
                          "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings) and exit")
@@ -213,31 +216,44 @@ def main(argv=None) -> int:
     out = torch.empty_like(d.q)
     lse = torch.empty(d.q.shape[:2], dtype=torch.float32, device=d.q.device)
     stream = torch.cuda.current_stream()
+    side = torch.cuda.Stream() if args.streams == 2 else stream
     has_dec = work["decode_rows"] > 0
     has_pre = work["prefill_chunks"] > 0
+    two = args.streams == 2 and has_dec and has_pre
 
     def step(ev=None):
+        """append; then decode half and prefill half (concurrently with two
+        streams). Events: 0 step start, 1 append done, 2 decode done (on the
+        main stream), 3 prefill done (on its stream), 4 step done."""
         if ev:
             ev[0].record(stream)
         mpa.kv_append(d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
                       d.seq_lens_host, d.qsl_host, stream=stream)
         if ev:
             ev[1].record(stream)
+        pre_stream = stream
+        if two:
+            side.wait_stream(stream)
+            pre_stream = side
+        if has_pre:
+            mpa.prefill_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
+                                  d.seq_lens_host, d.qsl_host, out, lse=lse, scale=d.scale, stream=pre_stream)
+        if ev:
+            ev[3].record(pre_stream)
         if has_dec:
             mpa.decode_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
                                  d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws, scale=d.scale,
                                  stream=stream)
         if ev:
             ev[2].record(stream)
-        if has_pre:
-            mpa.prefill_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
-                                  d.seq_lens_host, d.qsl_host, out, lse=lse, scale=d.scale, stream=stream)
+        if two:
+            stream.wait_stream(side)
         if ev:
-            ev[3].record(stream)
+            ev[4].record(stream)
 
     for _ in range(args.warmup):
         step()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
@@ -248,7 +264,9 @@ def main(argv=None) -> int:
     def avg_ms(a, b):
         return float(np.mean([e[a].elapsed_time(e[b]) for e in events]))
 
-    phase_ms = {"append": avg_ms(0, 1), "decode": avg_ms(1, 2), "prefill": avg_ms(2, 3)}
+    # With one stream the halves run prefill-then-decode; with two they overlap.
+    phase_ms = {"append": avg_ms(0, 1), "decode": avg_ms(3, 2) if not two else avg_ms(1, 2),
+                "prefill": avg_ms(1, 3), "step": avg_ms(0, 4)}
     ms_per_step = wall * 1e3 / args.steps
     value = work["query_tokens"] * args.steps / wall
     dec_gbs = work["decode_bytes"] / (phase_ms["decode"] * 1e-3) / 1e9 if has_dec else None
@@ -260,7 +278,7 @@ def main(argv=None) -> int:
         kernel = "decode_kernel+merge_kernel"
     else:
         achieved, peak, unit, bound = pre_tflops, MFMA_BF16_PEAK_TFLOPS, "TFLOP/s", "mfma"
-        kernel = "prefill_kernel"
+        kernel = "prefill_mfma_kernel"
     roofline = {
         "bound": bound,
         "achieved": round(achieved, 2),
@@ -287,7 +305,7 @@ def main(argv=None) -> int:
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) values, shuffled block tables)",
-        "config": {"workload": f"{args.config}: {WORKLOADS[args.config]}", "seed": args.seed,
+        "config": {"workload": f"{args.config}: {WORKLOADS[args.config]}", "seed": args.seed, "streams": args.streams if two else 1,
                    "decode_rows": work["decode_rows"], "prefill_chunks": work["prefill_chunks"],
                    "query_tokens": work["query_tokens"], "parallelism": "single GPU"},
         "roofline": roofline,

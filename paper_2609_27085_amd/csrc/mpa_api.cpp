@@ -203,6 +203,7 @@ int mpa_kv_append(const mpa_shape* shape, const void* k_new, const void* v_new, 
       acc += ql;
     }
     p.tok_start[c1 - c0] = acc;
+    p.unit = acc == (int)(c1 - c0) ? 1 : 0;
     hipError_t e = mpa::launch_append(a, p, shape->dtype, shape->head_dim, (hipStream_t)stream);
     if (e != hipSuccess) return MPA_ERR_HIP;
   }

@@ -65,6 +65,8 @@ struct AppendArgs {
 // row0[j] + (k - tok_start[j]) at position pos0[j] + (k - tok_start[j]).
 struct AppendPlan {
   int32_t n_seqs;
+  int32_t unit;  // 1 when every sequence of the plan adds exactly one token
+
   int32_t seq[kMaxPlanSeqs];
   int32_t row0[kMaxPlanSeqs];
   int32_t pos0[kMaxPlanSeqs];

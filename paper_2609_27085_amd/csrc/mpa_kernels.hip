@@ -253,11 +253,13 @@ __device__ inline void consume_block(const AttnArgs& a, const typename Tr<DT>::C
 
 // Blocks kb_begin .. kb_end-1 for 16 rows whose smallest causal limit is
 // min_limit.  Software-pipelined one block deep: the next block's fragments
-// are requested before the current one is consumed (the request is pinned
-// in place with a scheduling barrier, and is issued unconditionally -- the
-// last block is requested twice -- so consuming a block waits only for its
-// own loads).  Block ids come from a coalesced load of up to 64 consecutive
-// block-table entries, one per lane, broadcast with readlane.
+// are requested before the current one is consumed (the request is pinned in
+// place with a scheduling barrier, and is issued unconditionally -- the last
+// block is requested twice -- so consuming a block waits only for its own
+// loads).  One block deep keeps the decode kernel at 3 waves per SIMD; two
+// deep costs a wave per SIMD and measured slower.  Block ids come from a
+// coalesced load of up to 64 consecutive block-table entries, one per lane,
+// broadcast with readlane.
 template <int DT, int D>
 __device__ inline void attend_blocks(const AttnArgs& a, const typename Tr<DT>::Chunk* qf,
                                      const int32_t* bt, int g, int kb_begin, int kb_end, int kend,
@@ -267,7 +269,7 @@ __device__ inline void attend_blocks(const AttnArgs& a, const typename Tr<DT>::C
     const int c1 = min(kb_end, c0 + 64);
     const int ids = c0 + lane < c1 ? bt[c0 + lane] : 0;
     auto block_id = [&](int kb) -> int {
-      int blk = __builtin_amdgcn_readlane(ids, kb - c0);
+      int blk = __builtin_amdgcn_readlane(ids, min(kb, c1 - 1) - c0);
       if (blk < 0 || blk >= a.nb) {
         poison = true;
         blk = 0;
@@ -278,11 +280,11 @@ __device__ inline void attend_blocks(const AttnArgs& a, const typename Tr<DT>::C
     BlockFrags<DT, D> fa, fb;
     load_block<DT, D>(a, block_id(c0), g, fa);
     for (int kb = c0; kb < c1; kb += 2) {
-      load_block<DT, D>(a, block_id(min(kb + 1, c1 - 1)), g, fb);
+      load_block<DT, D>(a, block_id(kb + 1), g, fb);
       __builtin_amdgcn_sched_barrier(0);
       consume_block<DT, D>(a, qf, fa, kb, kend, limit, is_edge(kb), st);
       if (kb + 1 >= c1) break;
-      load_block<DT, D>(a, block_id(min(kb + 2, c1 - 1)), g, fa);
+      load_block<DT, D>(a, block_id(kb + 2), g, fa);
       __builtin_amdgcn_sched_barrier(0);
       consume_block<DT, D>(a, qf, fb, kb + 1, kend, limit, is_edge(kb + 1), st);
     }
@@ -357,15 +359,15 @@ __global__ __launch_bounds__(256) void decode_kernel(AttnArgs a, DecodePlan p) {
 // Split-K merge: one 64-lane workgroup per (decode sequence, query head).
 // With split maxima m_j and sums l_j (log2 units), the row's softmax
 // denominator is sum_j l_j 2^(m_j - M) with M = max_j m_j, and its output is
-// sum_j acc_j 2^(m_j - M) divided by that denominator.  Lanes load the
-// (m_j, l_j) of 64 splits at once; the weights go through LDS and every lane
-// then accumulates D/64 output dims over the splits with independent loads.
+// sum_j acc_j 2^(m_j - M) divided by that denominator.  Splits are taken 16
+// at a time with every load of a group issued before any is used, so a group
+// costs one memory latency.
 template <int DT, int D>
 __global__ __launch_bounds__(64) void merge_kernel(AttnArgs a, DecodePlan p) {
   using T = Tr<DT>;
   using E = typename T::Elem;
   constexpr int PER = D / 64;
-  __shared__ float w_s[64];
+  constexpr int GRP = 16;
   const int lane = threadIdx.x;
   const int j = blockIdx.x;
   const int h = blockIdx.y;
@@ -374,37 +376,39 @@ __global__ __launch_bounds__(64) void merge_kernel(AttnArgs a, DecodePlan p) {
   if (n <= 1) return;
   const int s = p.seq[j];
   const size_t base = (size_t)p.item_base + p.item_start[j];
-  float M = -INFINITY;
-  for (int i = lane; i < n; i += 64) M = fmaxf(M, a.ws_ml[((base + i) * a.hq + h) * 2]);
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
-  float lsum = 0.f;
+  const size_t stride = (size_t)a.hq * D;
+  const float* ml = a.ws_ml + (base * a.hq + h) * 2;
+  const float* acc = a.ws_o + (base * a.hq + h) * D + lane;
+  float M = -INFINITY, lsum = 0.f;
   float o[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) o[e] = 0.f;
-  for (int c0 = 0; c0 < n; c0 += 64) {
-    const int i = c0 + lane;
-    float w = 0.f;
-    if (i < n) {
-      const size_t slot = (base + i) * a.hq + h;
-      w = exp2_fast(a.ws_ml[slot * 2] - M);
-      lsum += w * a.ws_ml[slot * 2 + 1];
-    }
-    __syncthreads();
-    w_s[lane] = w;
-    __syncthreads();
-    const int cnt = min(64, n - c0);
-    const float* acc = a.ws_o + ((base + c0) * a.hq + h) * D + lane;
-    const size_t stride = (size_t)a.hq * D;
-#pragma unroll 8
-    for (int k = 0; k < cnt; ++k) {
-      const float wk = w_s[k];
+  for (int c0 = 0; c0 < n; c0 += GRP) {
+    float mj[GRP], lj[GRP], vj[GRP][PER];
 #pragma unroll
-      for (int e = 0; e < PER; ++e) o[e] += wk * acc[k * stride + 64 * e];
+    for (int k = 0; k < GRP; ++k) {
+      const int i = min(c0 + k, n - 1);  // past the end: a repeat, weighted 0 below
+      mj[k] = ml[(size_t)i * a.hq * 2];
+      lj[k] = ml[(size_t)i * a.hq * 2 + 1];
+#pragma unroll
+      for (int e = 0; e < PER; ++e) vj[k][e] = acc[i * stride + 64 * e];
     }
+    float gm = M;
+#pragma unroll
+    for (int k = 0; k < GRP; ++k) gm = fmaxf(gm, mj[k]);
+    const float rescale = exp2_fast(M - gm);  // M = -inf on the first group: 0
+    lsum *= rescale;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) o[e] *= rescale;
+#pragma unroll
+    for (int k = 0; k < GRP; ++k) {
+      const float w = c0 + k < n ? exp2_fast(mj[k] - gm) : 0.f;
+      lsum += w * lj[k];
+#pragma unroll
+      for (int e = 0; e < PER; ++e) o[e] += w * vj[k][e];
+    }
+    M = gm;
   }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) lsum += __shfl_xor(lsum, off);
   const int t = a.qsl[s];
   E* out = reinterpret_cast<E*>(a.out) + ((size_t)t * a.hq + h) * D;
   const float inv = 1.f / lsum;
@@ -724,19 +728,22 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
 
 // ---------------------------------------------------------------------------
 // Append: one wave per new token.  The token's sequence comes from the
-// kernel-argument plan (a scalar binary search), its block id from one scalar
-// load; the wave then copies the token's Hkv*d key elements as 16-byte
-// chunks and its value elements into the V^T rows of the slot.
+// kernel-argument plan (directly when every sequence of the plan adds one
+// token, else by a scalar binary search), its block id from one scalar load;
+// the wave then copies the token's Hkv*d key elements as 16-byte chunks and
+// its value elements into the V^T rows of the slot, issuing the loads of up
+// to 4 chunks per lane before their stores.
 template <int DT, int D>
 __global__ __launch_bounds__(256) void append_kernel(AppendArgs a, AppendPlan p) {
   using T = Tr<DT>;
   using E = typename T::Elem;
   constexpr int X = T::X;
   constexpr int NC = D / X;
+  constexpr int U = 4;
   const int lane = threadIdx.x & 63;
   const int tok = blockIdx.x * kWavesPerGroup + wave_uniform(threadIdx.x >> 6);
   if (tok >= p.tok_start[p.n_seqs]) return;
-  const int j = upper_index(p.tok_start, p.n_seqs, tok);
+  const int j = p.unit ? tok : upper_index(p.tok_start, p.n_seqs, tok);
   const int k = tok - p.tok_start[j];
   const int s = p.seq[j];
   const int t = p.row0[j] + k;
@@ -744,20 +751,30 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a, AppendPlan p)
   const int blk = a.block_tables[(size_t)s * a.mb + pos / kBlock];
   if (blk < 0 || blk >= a.nb) return;
   const int slot = pos % kBlock;
-  for (int ci = lane; ci < a.hkv * NC; ci += 64) {
-    const int h = ci / NC;
-    const int c = ci - h * NC;
-    const size_t head = (size_t)blk * a.hkv + h;
-    const E* kn = reinterpret_cast<const E*>(a.k_new) + ((size_t)t * a.hkv + h) * D + c * X;
-    E* kc = reinterpret_cast<E*>(a.k_cache) + ((head * NC + c) * kBlock + slot) * X;
-    *reinterpret_cast<u32x4*>(kc) = *reinterpret_cast<const u32x4*>(kn);
-    const E* vn = reinterpret_cast<const E*>(a.v_new) + ((size_t)t * a.hkv + h) * D + c * X;
-    E* vc = reinterpret_cast<E*>(a.v_cache) + (head * D + c * X) * kBlock + slot;
-    E vv[X];
+  const int nchunk = a.hkv * NC;
+  for (int c0 = 0; c0 < nchunk; c0 += 64 * U) {
+    u32x4 kv[U];
+    E vv[U][X];
 #pragma unroll
-    for (int e = 0; e < X; ++e) vv[e] = vn[e];
+    for (int u = 0; u < U; ++u) {
+      const int ci = min(c0 + 64 * u + lane, nchunk - 1);
+      const int h = ci / NC, c = ci - h * NC;
+      const size_t src = ((size_t)t * a.hkv + h) * D + c * X;
+      kv[u] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const E*>(a.k_new) + src);
 #pragma unroll
-    for (int e = 0; e < X; ++e) vc[e * kBlock] = vv[e];
+      for (int e = 0; e < X; ++e) vv[u][e] = reinterpret_cast<const E*>(a.v_new)[src + e];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int ci = c0 + 64 * u + lane;
+      if (ci >= nchunk) continue;
+      const int h = ci / NC, c = ci - h * NC;
+      const size_t head = (size_t)blk * a.hkv + h;
+      *reinterpret_cast<u32x4*>(reinterpret_cast<E*>(a.k_cache) + ((head * NC + c) * kBlock + slot) * X) = kv[u];
+      E* vc = reinterpret_cast<E*>(a.v_cache) + (head * D + c * X) * kBlock + slot;
+#pragma unroll
+      for (int e = 0; e < X; ++e) vc[e * kBlock] = vv[u][e];
+    }
   }
 }
 
