@@ -644,6 +644,17 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
     if (wave_active && key_base < w_kend) {
       const uint16_t* K = sk + (kt % STAGES) * TILE;
       const uint16_t* V = sv + (kt % STAGES) * TILE;
+      // All K operands of the tile are read from LDS before the first MFMA,
+      // so the reads' latency overlaps instead of separating every MFMA pair
+      // (left to itself the scheduler reuses one register quad for them all).
+      bf16x8 kf[2][KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+          kf[rt][ks] =
+              __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(K + 2 * rt * BLK + koff + (2 * ks + h) * 128));
+      __builtin_amdgcn_sched_barrier(0);
       f32x16 st[2];
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt)
@@ -654,11 +665,17 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt) {
-          const bf16x8 kf =
-              __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(K + 2 * rt * BLK + koff + (2 * ks + h) * 128));
-          st[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], st[rt], 0, 0, 0);
-        }
+        for (int rt = 0; rt < 2; ++rt)
+          st[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[rt][ks], qf[ks], st[rt], 0, 0, 0);
+      // V operands: issued now, they land while the softmax runs
+      bf16x8 vf[4][DT];
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          vf[t][dt] = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const u32x4*>(V + t * BLK + (h * D + n) * 8 + 32 * dt * 8));
+      __builtin_amdgcn_sched_barrier(0);
       if (key_base + BN - 1 > w_min_limit) {
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
@@ -695,14 +712,9 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
         }
       }
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const uint16_t* vbase = V + t * BLK + (h * D + n) * 8;
+      for (int t = 0; t < 4; ++t)
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          const bf16x8 vf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(vbase + 32 * dt * 8));
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[t], o[dt], 0, 0, 0);
-        }
-      }
+        for (int dt = 0; dt < DT; ++dt) o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[t][dt], pb[t], o[dt], 0, 0, 0);
     }
     // this wave's part of tile kt+1 has landed once only the copies issued
     // after it (tiles kt+2 .. kt+STAGES-1) remain in flight
