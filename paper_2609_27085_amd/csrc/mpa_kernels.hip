@@ -43,14 +43,15 @@ constexpr float kLn2 = 0.69314718055994530942f;
 __device__ inline int wave_uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 __device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// max(x[lane], x[lane ^ 32]) with one VALU lane swap (no LDS round trip, so
+// no wait on outstanding LDS reads)
+__device__ inline float max_across_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 __device__ inline short bf16_bits(float x) { return __builtin_bit_cast(short, (__bf16)x); }
 
-// 16 bytes per lane from global memory straight into LDS: lane l's bytes land
-// at lds + 16*l (lds must be the same for the whole wave).  Issued as inline
-// assembly so that the compiler does not make every later LDS read wait for
-// it (it cannot tell that the read targets another buffer); the caller waits
-// with an explicit vector-memory wait before the barrier that publishes the
-// tile.  M0 is written only here in this file.
 // s_waitcnt immediate that waits until at most n vector-memory operations are
 // outstanding (expcnt and lgkmcnt left at their maxima).  Used through the
 // intrinsic, which the compiler's own wait-count tracking understands.
@@ -61,6 +62,12 @@ constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) |
     asm volatile("" ::: "memory");                 \
   } while (0)
 
+// 16 bytes per lane from global memory straight into LDS: lane l's bytes land
+// at lds + 16*l (lds must be the same for the whole wave).  Issued as inline
+// assembly so that the compiler does not make every later LDS read wait for
+// it (it cannot tell that the read targets another buffer); the caller waits
+// with an explicit vector-memory wait before the barrier that publishes the
+// tile.  M0 is written only here in this file.
 __device__ inline void global_to_lds16(const void* g, void* lds) {
   const unsigned off = (unsigned)(size_t)(__attribute__((address_space(3))) void*)lds;
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(off) : "memory");
@@ -572,9 +579,10 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   // Tile kt's copy.  A block index past the sequence's last needed block is
   // clamped to it (its keys are all masked and its V entries zeroed), so
   // every copy is issued, always 2*WI instructions per wave per tile.
-  auto copy_tile = [&](int kt) -> int {
+  // the id of the block this wave copies for tile kt (a scalar load)
+  auto tile_block = [&](int kt) -> int { return bt[min(kt * NB + my_bi, nblk - 1)]; };
+  auto copy_tile = [&](int kt, int blk_raw) -> int {
     const int stage = kt % STAGES;
-    const int blk_raw = bt[min(kt * NB + my_bi, nblk - 1)];
     const int blk = (blk_raw >= 0 && blk_raw < a.nb) ? blk_raw : 0;
     const size_t gran = ((size_t)blk * a.hkv + g) * BLK;
 #pragma unroll
@@ -632,14 +640,19 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   // prologue: tiles 0 .. STAGES-2 in flight; tile 0 published
   int blk_id[STAGES];
 #pragma unroll
-  for (int k = 0; k < STAGES - 1; ++k) blk_id[k] = copy_tile(k);
+  for (int k = 0; k < STAGES - 1; ++k) blk_id[k] = copy_tile(k, tile_block(k));
+  // each iteration loads the block id the next one copies, after its last LDS
+  // read has been waited for (a scalar load shares the LDS wait counter and
+  // may complete out of order, so an earlier load would turn the MFMAs'
+  // partial waits into full ones); the closing barrier waits for it anyway
+  int next_blk = tile_block(STAGES - 1);
   MPA_WAIT_VMCNT(2 * WI * (STAGES - 2));
   fix_tile(0, blk_id[0]);
   __syncthreads();
 
   for (int kt = 0; kt < ntile; ++kt) {
     // copy tile kt+STAGES-1 into the stage tile kt-1 used (all waves are past it)
-    blk_id[(kt + STAGES - 1) % STAGES] = copy_tile(kt + STAGES - 1);
+    blk_id[(kt + STAGES - 1) % STAGES] = copy_tile(kt + STAGES - 1, next_blk);
     const int key_base = kt * BN;
     if (wave_active && key_base < w_kend) {
       const uint16_t* K = sk + (kt % STAGES) * TILE;
@@ -686,12 +699,13 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
             if (key > limit) st[rt][r] = -INFINITY;
           }
       }
-      float mx = -INFINITY;
+      // row maximum: four independent chains, then across the two lane halves
+      float m4[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[rt][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+        for (int r = 0; r < 16; ++r) m4[r & 3] = fmaxf(m4[r & 3], st[rt][r]);
+      const float mx = max_across_halves(fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3])));
       if (__any(mx > m_ref + thresh)) {
         const float m_new = fmaxf(m_ref, mx);
         const float alpha = m_new == -INFINITY ? 1.f : exp2_fast((m_ref - m_new) * c);
@@ -702,20 +716,24 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
       }
       const float mc = m_ref * c;
       bf16x8 pb[4];
+      float l4[4] = {0.f, 0.f, 0.f, 0.f};  // independent partial sums
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const float pv = exp2_fast(fmaf(st[t >> 1][8 * (t & 1) + e], c, -mc));
-          l += pv;
+          l4[e & 3] += pv;
           pb[t][e] = (__bf16)pv;
         }
       }
+      l += (l4[0] + l4[1]) + (l4[2] + l4[3]);
 #pragma unroll
       for (int t = 0; t < 4; ++t)
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[t][dt], pb[t], o[dt], 0, 0, 0);
     }
+    __builtin_amdgcn_sched_barrier(0);
+    next_blk = tile_block(kt + STAGES);
     // this wave's part of tile kt+1 has landed once only the copies issued
     // after it (tiles kt+2 .. kt+STAGES-1) remain in flight
     MPA_WAIT_VMCNT(2 * WI * (STAGES - 2));
