@@ -62,15 +62,19 @@ constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) |
     asm volatile("" ::: "memory");                 \
   } while (0)
 
-// 16 bytes per lane from global memory straight into LDS: lane l's bytes land
-// at lds + 16*l (lds must be the same for the whole wave).  Issued as inline
-// assembly so that the compiler does not make every later LDS read wait for
-// it (it cannot tell that the read targets another buffer); the caller waits
-// with an explicit vector-memory wait before the barrier that publishes the
-// tile.  M0 is written only here in this file.
-__device__ inline void global_to_lds16(const void* g, void* lds) {
+// 16 bytes per lane from global memory straight into LDS: lane l reads the
+// 16 bytes at base + voff (base uniform, held in SGPRs; voff the lane's byte
+// offset) and they land at lds + 16*l (lds the same for the whole wave).
+// With the base in SGPRs the per-lane offsets are loop invariant, so a copy
+// needs no per-copy address arithmetic in VGPRs (whose reuse would make each
+// copy wait for the previous one to be sent).  Issued as inline assembly so
+// that the compiler does not make every later LDS read wait for it (it cannot
+// tell that the read targets another buffer); the caller waits with an
+// explicit vector-memory wait before the barrier that publishes the tile.  M0
+// is written only here in this file.
+__device__ inline void global_to_lds16(const void* base, unsigned voff, void* lds) {
   const unsigned off = (unsigned)(size_t)(__attribute__((address_space(3))) void*)lds;
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(off) : "memory");
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "s"(off) : "memory");
 }
 
 // ---------------------------------------------------------------------------
@@ -585,6 +589,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
     const int stage = kt % STAGES;
     const int blk = (blk_raw >= 0 && blk_raw < a.nb) ? blk_raw : 0;
     const size_t gran = ((size_t)blk * a.hkv + g) * BLK;
+    const uint16_t* kbase = reinterpret_cast<const uint16_t*>(a.k_cache) + gran;
+    const uint16_t* vbase = reinterpret_cast<const uint16_t*>(a.v_cache) + gran;
 #pragma unroll
     for (int u = 0; u < WI; ++u) {
       const int ii = wave * WI + u;                 // 1 KB slice of the tile
@@ -592,12 +598,10 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
       // K: piece (chunk c, slot) <- key swap23(slot) of chunk c
       const int kc = cq >> 4, ks16 = cq & 15;
       const int kkey = (ks16 & 3) | ((ks16 & 4) << 1) | ((ks16 & 8) >> 1);
-      global_to_lds16(reinterpret_cast<const uint16_t*>(a.k_cache) + gran + (kc * 16 + kkey) * 8,
-                      sk + stage * TILE + ii * 512);
+      global_to_lds16(kbase, (unsigned)((kc * 16 + kkey) * 16), sk + stage * TILE + ii * 512);
       // V: piece (half vh, row d) <- keys 8vh..8vh+7 of V^T row d
       const int vh = cq / D, vd = cq % D;
-      global_to_lds16(reinterpret_cast<const uint16_t*>(a.v_cache) + gran + vd * kBlock + vh * 8,
-                      sv + stage * TILE + ii * 512);
+      global_to_lds16(vbase, (unsigned)((vd * kBlock + vh * 8) * 2), sv + stage * TILE + ii * 512);
     }
     return blk_raw;
   };
