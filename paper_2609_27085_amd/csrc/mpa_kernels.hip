@@ -645,18 +645,18 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   int blk_id[STAGES];
 #pragma unroll
   for (int k = 0; k < STAGES - 1; ++k) blk_id[k] = copy_tile(k, tile_block(k));
-  // each iteration loads the block id the next one copies, after its last LDS
-  // read has been waited for (a scalar load shares the LDS wait counter and
-  // may complete out of order, so an earlier load would turn the MFMAs'
-  // partial waits into full ones); the closing barrier waits for it anyway
+  // each iteration loads the block id the next one copies (see below)
   int next_blk = tile_block(STAGES - 1);
   MPA_WAIT_VMCNT(2 * WI * (STAGES - 2));
   fix_tile(0, blk_id[0]);
   __syncthreads();
 
   for (int kt = 0; kt < ntile; ++kt) {
-    // copy tile kt+STAGES-1 into the stage tile kt-1 used (all waves are past it)
-    blk_id[(kt + STAGES - 1) % STAGES] = copy_tile(kt + STAGES - 1, next_blk);
+    // tile kt+STAGES-1 is copied into the stage tile kt-1 used (all waves are
+    // past it): by an active wave between its first QK products, so that the
+    // copy instructions are issued while the matrix core is busy
+    const int cblk = next_blk;
+    blk_id[(kt + STAGES - 1) % STAGES] = cblk;
     const int key_base = kt * BN;
     if (wave_active && key_base < w_kend) {
       const uint16_t* K = sk + (kt % STAGES) * TILE;
@@ -680,10 +680,16 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
       // the two 32-key row tiles are independent accumulation chains:
       // interleave them so back-to-back MFMAs never wait on each other
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
+      for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
           st[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[rt][ks], qf[ks], st[rt], 0, 0, 0);
+        if (ks == 1) {
+          __builtin_amdgcn_sched_barrier(0);
+          copy_tile(kt + STAGES - 1, cblk);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
       // V operands: issued now, they land while the softmax runs
       bf16x8 vf[4][DT];
 #pragma unroll
@@ -693,6 +699,11 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
           vf[t][dt] = __builtin_bit_cast(
               bf16x8, *reinterpret_cast<const u32x4*>(V + t * BLK + (h * D + n) * 8 + 32 * dt * 8));
       __builtin_amdgcn_sched_barrier(0);
+      // the next copy's block id: a scalar load shares the LDS wait counter
+      // and may complete out of order, so issued here, after the last LDS
+      // read of the tile, it only turns the PV waits into full ones, by
+      // which time the V reads have long landed
+      next_blk = tile_block(kt + STAGES);
       if (key_base + BN - 1 > w_min_limit) {
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
@@ -735,9 +746,10 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
       for (int t = 0; t < 4; ++t)
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[t][dt], pb[t], o[dt], 0, 0, 0);
+    } else {
+      copy_tile(kt + STAGES - 1, cblk);
+      next_blk = tile_block(kt + STAGES);
     }
-    __builtin_amdgcn_sched_barrier(0);
-    next_blk = tile_block(kt + STAGES);
     // this wave's part of tile kt+1 has landed once only the copies issued
     // after it (tiles kt+2 .. kt+STAGES-1) remain in flight
     MPA_WAIT_VMCNT(2 * WI * (STAGES - 2));
