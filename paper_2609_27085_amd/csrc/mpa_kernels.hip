@@ -651,6 +651,11 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   fix_tile(0, blk_id[0]);
   __syncthreads();
 
+  // Waves w and w + WAVES/2 share a SIMD and run the same phases; the issue
+  // arbiter favours the older one, so the upper half finishes each tile
+  // last and the lower half waits for it at the barrier.  Raising the upper
+  // half's priority shortens that critical path.
+  if (wave >= WAVES / 2) __builtin_amdgcn_s_setprio(1);
   for (int kt = 0; kt < ntile; ++kt) {
     // tile kt+STAGES-1 is copied into the stage tile kt-1 used (all waves are
     // past it): by an active wave between its first QK products, so that the
