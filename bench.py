@@ -8,8 +8,13 @@ before timing starts.  Prints one JSON line:
 
   value          query tokens/s over the timed steps (T * steps / wall time)
   roofline       the dominant phase's algorithmic bytes (or FLOPs) per launch
-                 over its HIP-event-timed average duration, against the
-                 MI355X datasheet peak (HBM 8 TB/s, bf16 dense MFMA 2.5 PF)
+                 over its average duration, timed with HIP events around that
+                 phase in every timed step, against the MI355X datasheet peak
+                 (HBM 8 TB/s, bf16 dense MFMA 2.5 PF)
+  phases_ms      every phase's duration from an untimed calibration pass with
+                 events between all phases (each event record costs ~4 us of
+                 GPU time, so the timed steps carry only the two around the
+                 dominant phase)
   cpu_baseline   the CPU oracle, timed on a bounded sample of the same step
 
     python bench.py [--steps K] [--warmup W] [--config decode8b] [--seed 0]
@@ -222,15 +227,20 @@ def main(argv=None) -> int:
     two = args.streams == 2 and has_dec and has_pre
 
     def step(ev=None):
-        """append; then decode half and prefill half (concurrently with two
-        streams). Events: 0 step start, 1 append done, 2 decode done (on the
-        main stream), 3 prefill done (on its stream), 4 step done."""
-        if ev:
-            ev[0].record(stream)
+        """append; then prefill half and decode half (concurrently with two
+        streams).  ev maps a mark -- "start", "append", "prefill", "decode",
+        "end" -- to the event recorded there; marks absent from ev are not
+        recorded."""
+        ev = ev or {}
+
+        def mark(name, s):
+            if name in ev:
+                ev[name].record(s)
+
+        mark("start", stream)
         mpa.kv_append(d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
                       d.seq_lens_host, d.qsl_host, stream=stream)
-        if ev:
-            ev[1].record(stream)
+        mark("append", stream)
         pre_stream = stream
         if two:
             side.wait_stream(stream)
@@ -238,41 +248,53 @@ def main(argv=None) -> int:
         if has_pre:
             mpa.prefill_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
                                   d.seq_lens_host, d.qsl_host, out, lse=lse, scale=d.scale, stream=pre_stream)
-        if ev:
-            ev[3].record(pre_stream)
+        mark("prefill", pre_stream)
         if has_dec:
             mpa.decode_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
                                  d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws, scale=d.scale,
                                  stream=stream)
-        if ev:
-            ev[2].record(stream)
+        mark("decode", stream)
         if two:
             stream.wait_stream(side)
-        if ev:
-            ev[4].record(stream)
+        mark("end", stream)
+
+    def new_events(names):
+        return {n: torch.cuda.Event(enable_timing=True) for n in names}
+
+    # With one stream the halves run prefill-then-decode; with two they overlap.
+    spans = {"append": ("start", "append"), "prefill": ("append", "prefill"),
+             "decode": ("prefill", "decode") if not two else ("append", "decode"), "step": ("start", "end")}
+
+    def avg_ms(evs, span):
+        a, b = spans[span]
+        return float(np.mean([e[a].elapsed_time(e[b]) for e in evs]))
 
     for _ in range(args.warmup):
         step()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    # untimed calibration pass: every phase, to pick the dominant one
+    calib = [new_events(["start", "append", "prefill", "decode", "end"]) for _ in range(max(3, min(10, args.steps)))]
+    for e in calib:
+        step(e)
+    torch.cuda.synchronize()
+    phase_ms = {k: avg_ms(calib, k) for k in spans}
+    dom = "decode" if has_dec and (not has_pre or phase_ms["decode"] >= phase_ms["prefill"]) else "prefill"
+    dom_marks = list(spans[dom])
+
+    events = [new_events(dom_marks) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
         step(events[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-
-    def avg_ms(a, b):
-        return float(np.mean([e[a].elapsed_time(e[b]) for e in events]))
-
-    # With one stream the halves run prefill-then-decode; with two they overlap.
-    phase_ms = {"append": avg_ms(0, 1), "decode": avg_ms(3, 2) if not two else avg_ms(1, 2),
-                "prefill": avg_ms(1, 3), "step": avg_ms(0, 4)}
+    dom_ms = avg_ms(events, dom)
     ms_per_step = wall * 1e3 / args.steps
     value = work["query_tokens"] * args.steps / wall
-    dec_gbs = work["decode_bytes"] / (phase_ms["decode"] * 1e-3) / 1e9 if has_dec else None
-    pre_tflops = work["prefill_flops"] / (phase_ms["prefill"] * 1e-3) / 1e12 if has_pre else None
-    # dominant phase: the one that takes longest
-    dom = "decode" if phase_ms["decode"] >= phase_ms["prefill"] else "prefill"
+    # the dominant phase from the timed steps, the other from the calibration pass
+    timed = dict(phase_ms)
+    timed[dom] = dom_ms
+    dec_gbs = work["decode_bytes"] / (timed["decode"] * 1e-3) / 1e9 if has_dec else None
+    pre_tflops = work["prefill_flops"] / (timed["prefill"] * 1e-3) / 1e12 if has_pre else None
     if dom == "decode":
         achieved, peak, unit, bound = dec_gbs, HBM_PEAK_GBS, "GB/s", "hbm"
         kernel = "decode_kernel+merge_kernel"
@@ -287,7 +309,7 @@ def main(argv=None) -> int:
         "frac": round(achieved / peak, 4),
         "traffic": measured_traffic(args.config, dom),
         "kernel": kernel,
-        "phase_ms": round(phase_ms[dom], 4),
+        "phase_ms": round(dom_ms, 4),
         "algorithmic_per_launch": work[f"{dom}_bytes"] if dom == "decode" else work["prefill_flops"],
     }
     total_bytes = work["decode_bytes"] + work["prefill_bytes"] + work["append_bytes"]
