@@ -510,8 +510,8 @@ __global__ __launch_bounds__(256) void prefill_kernel(AttnArgs a, PrefillPlan p)
 //    order: [block][d/8 chunks][slot][8], slot s = key swap23(s);
 //  * LDS holds V^T as [block][key half h][d][8 keys], so lane (m, h) of a PV
 //    step reads row 32dt+m of half h.
-// Each wave copies whole blocks of a tile, so it reads one block id per tile
-// (a scalar load) and fixes up its own pieces (zeroing V entries of keys >= L,
+// Each wave copies a contiguous part of one block of a tile, so it needs one
+// block id per tile (a scalar load) and fixes up its own pieces (zeroing V entries of keys >= L,
 // which may hold NaN/Inf; NaN for an invalid block id) before the barrier
 // that publishes the tile.
 //
