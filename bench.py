@@ -89,8 +89,16 @@ def algorithmic_work(seq_lens, qsl, hq, hkv, d, elem_bytes, block=16):
 
 
 def kernel_source_sha() -> str:
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the kernel source with comments and blank lines removed, so
+    that a comment-only edit keeps the recorded counters valid."""
+    import re
+
+    with open(KERNEL_SOURCE, encoding="utf-8") as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    lines = [re.sub(r"//.*$", "", ln).rstrip() for ln in text.splitlines()]
+    code = "\n".join(ln for ln in lines if ln.strip())
+    return hashlib.sha256(code.encode()).hexdigest()[:16]
 
 
 def measured_traffic(workload: str, phase: str):
