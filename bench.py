@@ -255,7 +255,8 @@ def main(argv=None) -> int:
             pre_stream = side
         if has_pre:
             mpa.prefill_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
-                                  d.seq_lens_host, d.qsl_host, out, lse=lse, scale=d.scale, stream=pre_stream)
+                                  d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws, scale=d.scale,
+                                  stream=pre_stream)
         mark("prefill", pre_stream)
         if has_dec:
             mpa.decode_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,

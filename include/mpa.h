@@ -123,8 +123,11 @@ int mpa_kv_append(const mpa_shape* shape, const void* k_new, const void* v_new, 
 
 /*
  * Bytes of device workspace that mpa_mixed_paged_attention needs for this
- * batch (the split-K partial results of long decode rows).  Depends only on
- * the shape and the host metadata.  Returns 0 for an invalid batch.
+ * batch: the split-K partial results of long decode rows, and of prefill
+ * chunks whose cached prefix is split across workgroups (short bf16 chunks
+ * on long prefixes, when the batch's prefill tiles alone would leave most of
+ * the device idle).  Depends only on the shape and the host metadata.
+ * Returns 0 for an invalid batch, and when nothing is split.
  */
 size_t mpa_workspace_size(const mpa_shape* shape, const int32_t* seq_lens_host,
                           const int32_t* query_start_loc_host);
@@ -143,7 +146,8 @@ size_t mpa_workspace_size(const mpa_shape* shape, const int32_t* seq_lens_host,
  * this is standard scaled dot-product attention under the causal rule above.
  *
  * Decode rows (q_len = 1) run as split-K over KV blocks with an LSE merge;
- * prefill chunks (q_len > 1) run as causal MFMA tiles.
+ * prefill chunks (q_len > 1) run as causal MFMA tiles, their cached prefix
+ * also split (and merged the same way) when the chunks are short.
  *
  * q                 device [T][Hq][d]
  * out               device [T][Hq][d], written for every row of every
@@ -163,12 +167,13 @@ int mpa_mixed_paged_attention(const mpa_shape* shape, const void* q, const void*
 /*
  * The two halves of mpa_mixed_paged_attention, for callers that time them
  * separately or run them on two streams: mpa_decode_attention computes only
- * the rows of sequences with q_len == 1 (split-K + merge; it alone needs the
- * workspace), mpa_prefill_attention only the rows of sequences with
- * q_len > 1.  Arguments and contracts are those of
- * mpa_mixed_paged_attention; both halves read the whole batch's metadata, so
- * running both gives results bit-identical to the mixed call.  The two
- * write disjoint rows of out and lse and may run concurrently.
+ * the rows of sequences with q_len == 1, mpa_prefill_attention only the rows
+ * of sequences with q_len > 1.  Arguments and contracts are those of
+ * mpa_mixed_paged_attention (the workspace is sized for the whole batch by
+ * mpa_workspace_size; each half uses its own disjoint part of it); both
+ * halves read the whole batch's metadata, so running both gives results
+ * bit-identical to the mixed call.  The two write disjoint rows of out and
+ * lse and disjoint workspace, and may run concurrently.
  */
 int mpa_decode_attention(const mpa_shape* shape, const void* q, const void* k_cache, const void* v_cache,
                          const int32_t* block_tables, const int32_t* seq_lens, const int32_t* query_start_loc,
@@ -179,7 +184,8 @@ int mpa_decode_attention(const mpa_shape* shape, const void* q, const void* k_ca
 int mpa_prefill_attention(const mpa_shape* shape, const void* q, const void* k_cache, const void* v_cache,
                           const int32_t* block_tables, const int32_t* seq_lens, const int32_t* query_start_loc,
                           const int32_t* seq_lens_host, const int32_t* query_start_loc_host,
-                          const int32_t* block_tables_host, void* out, float* lse, void* stream);
+                          const int32_t* block_tables_host, void* out, float* lse, void* workspace,
+                          size_t workspace_bytes, void* stream);
 
 /* Static description of a status code. */
 const char* mpa_status_string(int status);
@@ -193,8 +199,9 @@ typedef struct {
   int32_t num_prefill_seqs;  /* sequences with q_len > 1 */
   int32_t split_tokens;      /* KV tokens per decode split */
   int32_t num_decode_items;  /* (sequence, split) work items */
-  int32_t num_prefill_tiles; /* (sequence, query tile, KV head) work items */
+  int32_t num_prefill_tiles; /* (sequence, query tile, KV split, KV head) work items */
   int32_t decode_launches;   /* decode kernel launches (sequence chunks) */
+  int32_t prefill_max_splits; /* most KV splits of any prefill chunk (0: no chunk) */
 } mpa_plan_info;
 
 int mpa_get_plan_info(const mpa_shape* shape, const int32_t* seq_lens_host,

@@ -76,6 +76,7 @@ class MpaPlanInfo(ctypes.Structure):
         ("num_decode_items", ctypes.c_int32),
         ("num_prefill_tiles", ctypes.c_int32),
         ("decode_launches", ctypes.c_int32),
+        ("prefill_max_splits", ctypes.c_int32),
     ]
 
 
@@ -100,7 +101,7 @@ def lib() -> ctypes.CDLL:
         L.mpa_decode_attention.restype = ctypes.c_int
         L.mpa_decode_attention.argtypes = L.mpa_mixed_paged_attention.argtypes
         L.mpa_prefill_attention.restype = ctypes.c_int
-        L.mpa_prefill_attention.argtypes = [_SHP, _P, _P, _P, _P, _P, _P, _I32P, _I32P, _I32P, _P, _P, _P]
+        L.mpa_prefill_attention.argtypes = L.mpa_mixed_paged_attention.argtypes
         L.mpa_workspace_size.restype = ctypes.c_size_t
         L.mpa_workspace_size.argtypes = [_SHP, _I32P, _I32P]
         L.mpa_status_string.restype = ctypes.c_char_p
@@ -214,8 +215,7 @@ def _attention(which, q, k_cache, v_cache, block_tables, seq_lens, query_start_l
     shape = shape_of(q, k_cache, block_tables, sl, scale)
     args = [ctypes.byref(shape), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_tables), _ptr(seq_lens),
             _ptr(query_start_loc), _i32p(sl), _i32p(qs), _i32p(bth), _ptr(out), _ptr(lse)]
-    if which != "mpa_prefill_attention":
-        args += [None, 0] if workspace is None else [_ptr(workspace), workspace.numel() * workspace.element_size()]
+    args += [None, 0] if workspace is None else [_ptr(workspace), workspace.numel() * workspace.element_size()]
     args.append(_stream(stream))
     rc = getattr(lib(), which)(*args)
     if rc != MPA_OK:
@@ -237,7 +237,7 @@ def decode_attention(q, k_cache, v_cache, block_tables, seq_lens, query_start_lo
 
 
 def prefill_attention(q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host,
-                      out, lse=None, scale=None, block_tables_host=None, stream=None) -> None:
+                      out, lse=None, workspace=None, scale=None, block_tables_host=None, stream=None) -> None:
     """mpa_prefill_attention: only the rows of sequences with q_len > 1."""
     _attention("mpa_prefill_attention", q, k_cache, v_cache, block_tables, seq_lens, query_start_loc,
-               seq_lens_host, qsl_host, out, lse, None, scale, block_tables_host, stream)
+               seq_lens_host, qsl_host, out, lse, workspace, scale, block_tables_host, stream)

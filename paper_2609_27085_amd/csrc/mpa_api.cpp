@@ -115,9 +115,61 @@ int q_tile(const mpa_shape* sh) {
   return rows / (sh->num_q_heads / sh->num_kv_heads);
 }
 
+// Launch errors are read with hipGetLastError() after each launch.  That
+// call also returns an error left behind by an earlier runtime call on this
+// thread that nobody collected -- e.g. hipErrorNotReady from another
+// library's stream or event query -- so it is cleared once, after
+// validation, before this call's first launch.
+void clear_stale_hip_error() { (void)hipGetLastError(); }
+
 size_t workspace_bytes(const mpa_shape* sh, long items) {
   const size_t per = (size_t)sh->num_q_heads * (sh->head_dim + 2) * sizeof(float);
   return items * per;
+}
+
+// KV splits of the prefill chunks.  A chunk's query tiles times the KV heads
+// are its workgroups, and each workgroup holds a whole CU.  When the batch
+// has fewer than kPrefillSplitTarget of them (short chunks, e.g. a lease's
+// small token budget, on long cached prefixes) each chunk's prefix is divided
+// among up to `want` splits of about kPrefillMinSplitTiles 64-key tiles or
+// more; the last split also takes the chunk's own keys (and the causal
+// diagonal), so every split holds keys of every row.  bf16 only.
+struct PrefillSplit {
+  int nsplit = 1;
+  int tiles = 0;        // 64-key tiles of every split but the last
+  long item_base = 0;   // first workspace slot of the chunk's partials
+};
+
+std::vector<PrefillSplit> prefill_splits(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens,
+                                         const int32_t* qsl, long first_item) {
+  std::vector<PrefillSplit> out(b.prefill.size());
+  if (sh->dtype != MPA_BF16 || b.prefill.empty()) return out;
+  const int qt = q_tile(sh);
+  long units = 0;
+  for (int s : b.prefill) units += (long)(qsl[s + 1] - qsl[s] + qt - 1) / qt * sh->num_kv_heads;
+  if (units >= mpa::kPrefillSplitTarget) return out;
+  const int want = (int)((mpa::kPrefillSplitTarget + units - 1) / units);
+  long item = first_item;
+  for (size_t k = 0; k < b.prefill.size(); ++k) {
+    const int s = b.prefill[k];
+    const int C = qsl[s + 1] - qsl[s];
+    const int np = (seq_lens[s] - C) / 64;  // whole 64-key tiles of the prefix
+    const int ct = (C + 63) / 64;
+    const int n = std::min({want, 1 + np / mpa::kPrefillMinSplitTiles, 64});
+    if (n < 2) continue;
+    out[k].nsplit = n;
+    out[k].tiles = std::min((np + ct + n - 1) / n, np / (n - 1));
+    out[k].item_base = item;
+    item += (long)n * C;
+  }
+  return out;
+}
+
+long prefill_items(const std::vector<PrefillSplit>& sp, const Batch& b, const int32_t* qsl) {
+  long n = 0;
+  for (size_t k = 0; k < sp.size(); ++k)
+    if (sp[k].nsplit > 1) n += (long)sp[k].nsplit * (qsl[b.prefill[k] + 1] - qsl[b.prefill[k]]);
+  return n;
 }
 
 }  // namespace
@@ -148,8 +200,16 @@ int mpa_get_plan_info(const mpa_shape* shape, const int32_t* seq_lens_host, cons
   info->num_decode_items = (int32_t)decode_items(shape, b, seq_lens_host, split);
   long tiles = 0;
   const int qt = q_tile(shape);
-  for (int s : b.prefill) tiles += (qsl_host[s + 1] - qsl_host[s] + qt - 1) / qt;
+  const std::vector<PrefillSplit> ps =
+      prefill_splits(shape, b, seq_lens_host, qsl_host, decode_items(shape, b, seq_lens_host, split));
+  int max_split = b.prefill.empty() ? 0 : 1;
+  for (size_t k = 0; k < b.prefill.size(); ++k) {
+    const int s = b.prefill[k];
+    tiles += (long)(qsl_host[s + 1] - qsl_host[s] + qt - 1) / qt * ps[k].nsplit;
+    max_split = std::max(max_split, ps[k].nsplit);
+  }
   info->num_prefill_tiles = (int32_t)(tiles * shape->num_kv_heads);
+  info->prefill_max_splits = max_split;
   info->decode_launches = (int32_t)((b.decode.size() + mpa::kMaxPlanSeqs - 1) / mpa::kMaxPlanSeqs);
   return MPA_OK;
 }
@@ -160,8 +220,10 @@ size_t mpa_workspace_size(const mpa_shape* shape, const int32_t* seq_lens_host, 
   const int split = choose_split(shape, b, seq_lens_host);
   bool any_split = false;
   for (int s : b.decode) any_split |= seq_lens_host[s] > split;
-  if (!any_split) return 0;
-  return workspace_bytes(shape, decode_items(shape, b, seq_lens_host, split));
+  const long ditems = decode_items(shape, b, seq_lens_host, split);
+  const long pitems = prefill_items(prefill_splits(shape, b, seq_lens_host, qsl_host, ditems), b, qsl_host);
+  if (!any_split && pitems == 0) return 0;
+  return workspace_bytes(shape, ditems + pitems);
 }
 
 int mpa_kv_append(const mpa_shape* shape, const void* k_new, const void* v_new, void* k_cache, void* v_cache,
@@ -187,6 +249,7 @@ int mpa_kv_append(const mpa_shape* shape, const void* k_new, const void* v_new, 
   (void)query_start_loc;
   std::vector<int> seqs(b.decode);
   seqs.insert(seqs.end(), b.prefill.begin(), b.prefill.end());
+  clear_stale_hip_error();
   for (size_t c0 = 0; c0 < seqs.size(); c0 += mpa::kMaxPlanSeqs) {
     mpa::AppendPlan p;
     memset(&p, 0, sizeof(p));
@@ -231,12 +294,19 @@ int run_attention(int phases, const mpa_shape* shape, const void* q, const void*
     return MPA_ERR_INVALID;
   // The split size depends on every decode row of the batch, whichever
   // phase runs, so that the phases together equal the mixed call exactly.
+  // The workspace layout (decode partials, then prefill partials) is also
+  // the whole batch's, so the two halves can run concurrently.
   Batch all;
   check_batch(shape, seq_lens_host, query_start_loc_host, nullptr, false, &all);
   const int split = choose_split(shape, all, seq_lens_host);
-  const long items = decode_items(shape, b, seq_lens_host, split);
+  const long ditems = decode_items(shape, all, seq_lens_host, split);
+  const std::vector<PrefillSplit> psplit =
+      prefill_splits(shape, all, seq_lens_host, query_start_loc_host, ditems);
+  const long items = ditems + prefill_items(psplit, all, query_start_loc_host);
   bool any_split = false;
   for (int s : b.decode) any_split |= seq_lens_host[s] > split;
+  if (!b.prefill.empty())
+    for (const auto& ps : psplit) any_split |= ps.nsplit > 1;
   if (any_split) {
     const size_t need = workspace_bytes(shape, items);
     if (!workspace || workspace_bytes_given < need) return MPA_ERR_WORKSPACE;
@@ -258,6 +328,7 @@ int run_attention(int phases, const mpa_shape* shape, const void* q, const void*
   a.nb = shape->num_blocks;
   a.scale_log2 = shape->scale * 1.4426950408889634f;
   hipStream_t st = (hipStream_t)stream;
+  clear_stale_hip_error();
 
   // Decode rows, in launches of up to kMaxPlanSeqs sequences.
   std::vector<mpa::DecodePlan> dplans;
@@ -292,24 +363,37 @@ int run_attention(int phases, const mpa_shape* shape, const void* q, const void*
       if (e != hipSuccess) return MPA_ERR_HIP;
     }
   }
-  // Prefill chunks.
+  // Prefill chunks (b.prefill is all.prefill or empty), in launches of up to
+  // kMaxPrefillSeqs; KV-split chunks are merged after their launch.
   const int qt = q_tile(shape);
-  for (size_t c0 = 0; c0 < b.prefill.size(); c0 += mpa::kMaxPlanSeqs) {
+  for (size_t c0 = 0; c0 < b.prefill.size(); c0 += mpa::kMaxPrefillSeqs) {
     mpa::PrefillPlan p;
     memset(&p, 0, sizeof(p));
-    const size_t c1 = std::min(b.prefill.size(), c0 + mpa::kMaxPlanSeqs);
+    const size_t c1 = std::min(b.prefill.size(), c0 + mpa::kMaxPrefillSeqs);
     p.n_seqs = (int32_t)(c1 - c0);
     p.q_tile = qt;
-    int acc = 0;
+    int acc = 0, rows = 0;
     for (size_t k = c0; k < c1; ++k) {
       const int s = b.prefill[k];
+      const int C = query_start_loc_host[s + 1] - query_start_loc_host[s];
+      const PrefillSplit& ps = psplit[k];
       p.seq[k - c0] = s;
       p.tile_start[k - c0] = acc;
-      acc += (query_start_loc_host[s + 1] - query_start_loc_host[s] + qt - 1) / qt;
+      p.nsplit[k - c0] = ps.nsplit;
+      p.split_tiles[k - c0] = ps.tiles;
+      p.item_base[k - c0] = (int32_t)ps.item_base;
+      p.row_start[k - c0] = rows;
+      acc += (C + qt - 1) / qt * ps.nsplit;
+      if (ps.nsplit > 1) rows += C;
     }
     p.tile_start[c1 - c0] = acc;
+    p.row_start[c1 - c0] = rows;
     hipError_t e = mpa::launch_prefill(a, p, acc, shape->dtype, shape->head_dim, st);
     if (e != hipSuccess) return MPA_ERR_HIP;
+    if (rows > 0) {
+      e = mpa::launch_prefill_merge(a, p, shape->dtype, shape->head_dim, st);
+      if (e != hipSuccess) return MPA_ERR_HIP;
+    }
   }
   return MPA_OK;
 }
@@ -341,9 +425,11 @@ int mpa_decode_attention(const mpa_shape* shape, const void* q, const void* k_ca
 int mpa_prefill_attention(const mpa_shape* shape, const void* q, const void* k_cache, const void* v_cache,
                           const int32_t* block_tables, const int32_t* seq_lens, const int32_t* query_start_loc,
                           const int32_t* seq_lens_host, const int32_t* query_start_loc_host,
-                          const int32_t* block_tables_host, void* out, float* lse, void* stream) {
+                          const int32_t* block_tables_host, void* out, float* lse, void* workspace,
+                          size_t workspace_bytes_given, void* stream) {
   return run_attention(kPrefill, shape, q, k_cache, v_cache, block_tables, seq_lens, query_start_loc,
-                       seq_lens_host, query_start_loc_host, block_tables_host, out, lse, nullptr, 0, stream);
+                       seq_lens_host, query_start_loc_host, block_tables_host, out, lse, workspace,
+                       workspace_bytes_given, stream);
 }
 
 }  // extern "C"

@@ -11,6 +11,9 @@ namespace mpa {
 constexpr int kBlock = 16;            // tokens per cache block
 constexpr int kWavesPerGroup = 4;     // waves per workgroup in every kernel
 constexpr int kMaxPlanSeqs = 256;     // sequences per launch (kernel-argument plan)
+constexpr int kMaxPrefillSeqs = 64;   // prefill chunks per launch (its plan carries more per chunk)
+constexpr int kPrefillSplitTarget = 256;  // prefill workgroups a launch should at least have
+constexpr int kPrefillMinSplitTiles = 8;  // smallest KV range of a prefill split, in 64-key tiles
 constexpr int kPrefillRows = 64;      // (token, head) rows per f32 prefill workgroup
 constexpr int kPrefillRowsMfma = 256; // (token, head) rows per bf16 prefill workgroup (8 waves)
 
@@ -42,13 +45,25 @@ struct DecodePlan {
   int32_t item_start[kMaxPlanSeqs + 1];
 };
 
-// Prefill work for up to kMaxPlanSeqs sequences: query tile k of this launch
-// is tile (k - tile_start[j]) of sequence seq[j]; grid.y is the KV head.
+// Prefill work for up to kMaxPrefillSeqs sequences.  Work unit k of this
+// launch belongs to chunk j with tile_start[j] <= k < tile_start[j+1]; with
+// u = k - tile_start[j] it is query tile u / nsplit[j] and KV split
+// u % nsplit[j] of sequence seq[j].  Split x of a chunk covers 64-key tiles
+// [x * split_tiles[j], (x + 1) * split_tiles[j]), the last split everything
+// from there to the end; all splits but the last lie inside the cached
+// prefix.  A chunk with nsplit > 1 writes per-split partial results for its
+// token i and split x to workspace slot item_base[j] + x * C + i, and the
+// merge launch combines them (grid.x runs over row_start, the chunks' token
+// counts summed over split chunks only).
 struct PrefillPlan {
   int32_t n_seqs;
-  int32_t q_tile;    // query tokens per tile = kPrefillRows / G
-  int32_t seq[kMaxPlanSeqs];
-  int32_t tile_start[kMaxPlanSeqs + 1];
+  int32_t q_tile;    // query tokens per tile = rows per workgroup / G
+  int32_t seq[kMaxPrefillSeqs];
+  int32_t tile_start[kMaxPrefillSeqs + 1];
+  int32_t nsplit[kMaxPrefillSeqs];
+  int32_t split_tiles[kMaxPrefillSeqs];
+  int32_t item_base[kMaxPrefillSeqs];
+  int32_t row_start[kMaxPrefillSeqs + 1];
 };
 
 struct AppendArgs {
@@ -83,5 +98,8 @@ hipError_t launch_decode(const AttnArgs& a, const DecodePlan& p, int n_items, in
 hipError_t launch_merge(const AttnArgs& a, const DecodePlan& p, int dtype, int head_dim, hipStream_t stream);
 hipError_t launch_prefill(const AttnArgs& a, const PrefillPlan& p, int n_tiles, int dtype, int head_dim,
                           hipStream_t stream);
+// Combines the KV-split partial results of the plan's split chunks.
+hipError_t launch_prefill_merge(const AttnArgs& a, const PrefillPlan& p, int dtype, int head_dim,
+                                hipStream_t stream);
 
 }  // namespace mpa

@@ -373,23 +373,20 @@ __global__ __launch_bounds__(256) void decode_kernel(AttnArgs a, DecodePlan p) {
 // sum_j acc_j 2^(m_j - M) divided by that denominator.  Splits are taken 16
 // at a time with every load of a group issued before any is used, so a group
 // costs one memory latency.
+// One output row from n split-K partial results: m_k (row maximum, log2
+// units), l_k (sum of exp2(s - m_k)) and acc_k (sum of exp2(s - m_k) v) are
+// combined with the weights exp2(m_k - max m), 16 splits at a time with all
+// of a group's loads issued before any is used.  ml points at split 0's
+// (m, l) pair, acc at split 0's element `lane` of the row; consecutive splits
+// are ml_stride and acc_stride floats apart.  Lane l writes elements l,
+// l + 64, ... of out; lane 0 writes lse.
 template <int DT, int D>
-__global__ __launch_bounds__(64) void merge_kernel(AttnArgs a, DecodePlan p) {
+__device__ inline void merge_splits(const float* ml, size_t ml_stride, const float* acc, size_t acc_stride, int n,
+                                    typename Tr<DT>::Elem* out, float* lse) {
   using T = Tr<DT>;
-  using E = typename T::Elem;
   constexpr int PER = D / 64;
   constexpr int GRP = 16;
-  const int lane = threadIdx.x;
-  const int j = blockIdx.x;
-  const int h = blockIdx.y;
-  if (j >= p.n_seqs) return;
-  const int n = p.item_start[j + 1] - p.item_start[j];
-  if (n <= 1) return;
-  const int s = p.seq[j];
-  const size_t base = (size_t)p.item_base + p.item_start[j];
-  const size_t stride = (size_t)a.hq * D;
-  const float* ml = a.ws_ml + (base * a.hq + h) * 2;
-  const float* acc = a.ws_o + (base * a.hq + h) * D + lane;
+  const int lane = threadIdx.x & 63;
   float M = -INFINITY, lsum = 0.f;
   float o[PER];
 #pragma unroll
@@ -399,10 +396,10 @@ __global__ __launch_bounds__(64) void merge_kernel(AttnArgs a, DecodePlan p) {
 #pragma unroll
     for (int k = 0; k < GRP; ++k) {
       const int i = min(c0 + k, n - 1);  // past the end: a repeat, weighted 0 below
-      mj[k] = ml[(size_t)i * a.hq * 2];
-      lj[k] = ml[(size_t)i * a.hq * 2 + 1];
+      mj[k] = ml[(size_t)i * ml_stride];
+      lj[k] = ml[(size_t)i * ml_stride + 1];
 #pragma unroll
-      for (int e = 0; e < PER; ++e) vj[k][e] = acc[i * stride + 64 * e];
+      for (int e = 0; e < PER; ++e) vj[k][e] = acc[(size_t)i * acc_stride + 64 * e];
     }
     float gm = M;
 #pragma unroll
@@ -420,12 +417,48 @@ __global__ __launch_bounds__(64) void merge_kernel(AttnArgs a, DecodePlan p) {
     }
     M = gm;
   }
-  const int t = a.qsl[s];
-  E* out = reinterpret_cast<E*>(a.out) + ((size_t)t * a.hq + h) * D;
   const float inv = 1.f / lsum;
 #pragma unroll
   for (int e = 0; e < PER; ++e) T::store1(out + lane + 64 * e, o[e] * inv);
-  if (a.lse && lane == 0) a.lse[(size_t)t * a.hq + h] = (M + log2f(lsum)) * kLn2;
+  if (lse && lane == 0) *lse = (M + log2f(lsum)) * kLn2;
+}
+
+// Decode merge: one 64-lane workgroup per (split decode sequence, q head).
+template <int DT, int D>
+__global__ __launch_bounds__(64) void merge_kernel(AttnArgs a, DecodePlan p) {
+  using E = typename Tr<DT>::Elem;
+  const int j = blockIdx.x;
+  const int h = blockIdx.y;
+  if (j >= p.n_seqs) return;
+  const int n = p.item_start[j + 1] - p.item_start[j];
+  if (n <= 1) return;
+  const int s = p.seq[j];
+  const size_t base = (size_t)p.item_base + p.item_start[j];
+  const int t = a.qsl[s];
+  merge_splits<DT, D>(a.ws_ml + (base * a.hq + h) * 2, (size_t)a.hq * 2,
+                      a.ws_o + (base * a.hq + h) * D + threadIdx.x, (size_t)a.hq * D, n,
+                      reinterpret_cast<E*>(a.out) + ((size_t)t * a.hq + h) * D,
+                      a.lse ? a.lse + (size_t)t * a.hq + h : nullptr);
+}
+
+// Prefill merge: one 64-lane workgroup per (token of a KV-split chunk, q
+// head); split x of token i of chunk j sits at slot item_base[j] + x*C + i.
+template <int DT, int D>
+__global__ __launch_bounds__(64) void prefill_merge_kernel(AttnArgs a, PrefillPlan p) {
+  using E = typename Tr<DT>::Elem;
+  const int r = blockIdx.x;
+  const int h = blockIdx.y;
+  if (r >= p.row_start[p.n_seqs]) return;
+  const int j = upper_index(p.row_start, p.n_seqs, r);
+  const int s = p.seq[j];
+  const int i = r - p.row_start[j];
+  const int t0 = a.qsl[s];
+  const int C = a.qsl[s + 1] - t0;
+  const size_t slot = (size_t)p.item_base[j] + i;
+  merge_splits<DT, D>(a.ws_ml + (slot * a.hq + h) * 2, (size_t)C * a.hq * 2,
+                      a.ws_o + (slot * a.hq + h) * D + threadIdx.x, (size_t)C * a.hq * D, p.nsplit[j],
+                      reinterpret_cast<E*>(a.out) + ((size_t)(t0 + i) * a.hq + h) * D,
+                      a.lse ? a.lse + (size_t)(t0 + i) * a.hq + h : nullptr);
 }
 
 // ---------------------------------------------------------------------------
@@ -544,7 +577,9 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   const int tile = n_tiles - 1 - (int)(blockIdx.x / a.hkv);  // last (longest) query tiles first
   const int j = upper_index(p.tile_start, p.n_seqs, tile);
   const int s = p.seq[j];
-  const int qt = tile - p.tile_start[j];
+  const int nsplit = p.nsplit[j];
+  const int qt = (tile - p.tile_start[j]) / nsplit;
+  const int split = tile - p.tile_start[j] - qt * nsplit;
   const int t0 = a.qsl[s];
   const int C = a.qsl[s + 1] - t0;
   const int L = a.seq_lens[s];
@@ -552,8 +587,10 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   const int G = a.hq / a.hkv;
   const int first_tok = qt * p.q_tile;
   const int last_tok = min(first_tok + p.q_tile - 1, C - 1);
-  const int kend = P + last_tok + 1;  // keys the workgroup needs
-  const int ntile = (kend + BN - 1) / BN;
+  const int kend = P + last_tok + 1;  // keys the query tile needs
+  // this workgroup's 64-key tiles: [kt_begin, ntile)
+  const int kt_begin = split * p.split_tiles[j];
+  const int ntile = split == nsplit - 1 ? (kend + BN - 1) / BN : kt_begin + p.split_tiles[j];
   cint* bt = (cint*)(a.block_tables + (size_t)s * a.mb);
 
   // this lane's query row
@@ -641,14 +678,14 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   // the Q fragments (ordinary loads) land before any tile copy is issued, so
   // that no wait inside the loop is ever needed for them
   MPA_WAIT_VMCNT(0);
-  // prologue: tiles 0 .. STAGES-2 in flight; tile 0 published
+  // prologue: the split's first STAGES-1 tiles in flight, its first published
   int blk_id[STAGES];
 #pragma unroll
-  for (int k = 0; k < STAGES - 1; ++k) blk_id[k] = copy_tile(k, tile_block(k));
+  for (int k = 0; k < STAGES - 1; ++k) blk_id[(kt_begin + k) % STAGES] = copy_tile(kt_begin + k, tile_block(kt_begin + k));
   // each iteration loads the block id the next one copies (see below)
-  int next_blk = tile_block(STAGES - 1);
+  int next_blk = tile_block(kt_begin + STAGES - 1);
   MPA_WAIT_VMCNT(2 * WI * (STAGES - 2));
-  fix_tile(0, blk_id[0]);
+  fix_tile(kt_begin, blk_id[kt_begin % STAGES]);
   __syncthreads();
 
   // Waves w and w + WAVES/2 share a SIMD and run the same phases; the issue
@@ -656,7 +693,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   // last and the lower half waits for it at the barrier.  Raising the upper
   // half's priority shortens that critical path.
   if (wave >= WAVES / 2) __builtin_amdgcn_s_setprio(1);
-  for (int kt = 0; kt < ntile; ++kt) {
+  for (int kt = kt_begin; kt < ntile; ++kt) {
     // tile kt+STAGES-1 is copied into the stage tile kt-1 used (all waves are
     // past it): by an active wave between its first QK products, so that the
     // copy instructions are issued while the matrix core is busy
@@ -765,6 +802,22 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
 
   const float lt = l + __shfl_xor(l, 32);
   if (!wave_active || !row_ok) return;
+  if (nsplit > 1) {  // partial result of this KV split, merged by prefill_merge_kernel
+    const size_t slot = ((size_t)p.item_base[j] + (size_t)split * C + i) * a.hq + head;
+    float* wo = a.ws_o + slot * D;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int jb = 0; jb < 4; ++jb) {
+        const f32x4 v4 = {o[dt][4 * jb], o[dt][4 * jb + 1], o[dt][4 * jb + 2], o[dt][4 * jb + 3]};
+        *reinterpret_cast<f32x4*>(wo + 32 * dt + 8 * jb + 4 * h) = v4;
+      }
+    if (h == 0) {
+      a.ws_ml[slot * 2] = m_ref * c;
+      a.ws_ml[slot * 2 + 1] = lt;
+    }
+    return;
+  }
   const float inv = 1.f / lt;
   uint16_t* out = reinterpret_cast<uint16_t*>(a.out) + ((size_t)(t0 + i) * a.hq + head) * D;
 #pragma unroll
@@ -941,6 +994,21 @@ hipError_t launch_decode(const AttnArgs& a, const DecodePlan& p, int n_items, in
 hipError_t launch_merge(const AttnArgs& a, const DecodePlan& p, int dtype, int head_dim, hipStream_t stream) {
   return dispatch<MergeL>(dtype, head_dim, a, p, stream);
 }
+template <int DT, int D>
+struct PrefillMergeL {
+  static hipError_t run(const AttnArgs& a, const PrefillPlan& p, hipStream_t stream) {
+    const int rows = p.row_start[p.n_seqs];
+    if (rows == 0) return hipSuccess;
+    hipLaunchKernelGGL((prefill_merge_kernel<DT, D>), dim3(rows, a.hq), dim3(64), 0, stream, a, p);
+    return hipGetLastError();
+  }
+};
+
+hipError_t launch_prefill_merge(const AttnArgs& a, const PrefillPlan& p, int dtype, int head_dim,
+                                hipStream_t stream) {
+  return dispatch<PrefillMergeL>(dtype, head_dim, a, p, stream);
+}
+
 hipError_t launch_prefill(const AttnArgs& a, const PrefillPlan& p, int n_tiles, int dtype, int head_dim,
                           hipStream_t stream) {
   return dispatch<PrefillL>(dtype, head_dim, a, p, n_tiles, stream);

@@ -129,6 +129,31 @@ def test_mixed_batches(torch_gpu, heads, dtype):
     check_batch(b, f"mixed {heads}")
 
 
+SPLIT_MIXES = [(8, 2, 64), (32, 8, 128), (16, 16, 128), (12, 4, 128), (16, 1, 64)]
+
+
+def split_specs(rng):
+    # short chunks on long cached prefixes: few query tiles, so the library
+    # splits each prefix across workgroups (some decode rows alongside)
+    specs = [SeqSpec(1500 + 100, 100), SeqSpec(2100 + 37, 37), SeqSpec(900 + 300, 300), SeqSpec(700 + 64, 64)]
+    specs += [SeqSpec(int(c), 1) for c in rng.integers(1, 3000, size=5)]
+    order = rng.permutation(len(specs))
+    return [specs[i] for i in order]
+
+
+@pytest.mark.parametrize("heads", SPLIT_MIXES, ids=lambda h: f"hq{h[0]}_hkv{h[1]}_d{h[2]}")
+def test_prefill_kv_splits(torch_gpu, heads):
+    rng = np.random.default_rng(40 + heads[1])
+    b = make_batch(split_specs(rng), HeadSpec(*heads, 16), "bf16", rng)
+    sh = mpa.make_shape(num_seqs=b.num_seqs, num_q_heads=heads[0], num_kv_heads=heads[1], head_dim=heads[2],
+                        num_blocks=b.num_blocks, max_blocks_per_seq=b.block_tables.shape[1],
+                        total_q_tokens=b.total_q, scale=b.scale, dtype=mpa.MPA_BF16)
+    info = mpa.plan_info(sh, b.seq_lens, b.query_start_loc)
+    say(f"[gpu] kv splits {heads}: up to {info.prefill_max_splits} splits, {info.num_prefill_tiles} workgroups")
+    assert info.prefill_max_splits > 1
+    check_batch(b, f"kv splits {heads}")
+
+
 def test_decode_only_and_prefill_only(torch_gpu):
     rng = np.random.default_rng(21)
     dec = [SeqSpec(int(c), 1) for c in rng.integers(1, 4000, size=20)]
@@ -200,13 +225,14 @@ def test_mixed_equals_parts(torch_gpu):
         assert torch.equal(l, l_all.index_select(0, rows))
 
 
-def test_phases_equal_mixed_call(torch_gpu):
+@pytest.mark.parametrize("specs", ["mixed", "split"])
+def test_phases_equal_mixed_call(torch_gpu, specs):
     """mpa_decode_attention then mpa_prefill_attention (here on two streams)
-    give the mixed call's bits."""
+    give the mixed call's bits, also when prefill chunks are KV-split."""
     import torch
 
     rng = np.random.default_rng(30)
-    b = make_batch(mixed_specs(rng), HeadSpec(32, 8, 128), "bf16", rng)
+    b = make_batch(mixed_specs(rng) if specs == "mixed" else split_specs(rng), HeadSpec(32, 8, 128), "bf16", rng)
     d = to_device(b)
     o_all, l_all = run_step(d)
     out = torch.full_like(d.q, float("nan"))
@@ -217,7 +243,7 @@ def test_phases_equal_mixed_call(torch_gpu):
     mpa.decode_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
                          d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws, scale=d.scale, stream=s1)
     mpa.prefill_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
-                          d.seq_lens_host, d.qsl_host, out, lse=lse, scale=d.scale, stream=s2)
+                          d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws, scale=d.scale, stream=s2)
     torch.cuda.synchronize()
     rows = torch.from_numpy(np.repeat(b.q_lens > 0, b.q_lens)).cuda()
     assert torch.equal(out[rows].view(torch.int16), o_all[rows].view(torch.int16))

@@ -30,6 +30,26 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(L, n), n
 
 
+def declared_arity():
+    """Parameter count of every function include/mpa.h declares."""
+    src = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    out = {}
+    for name, params in re.findall(r"\b(mpa_[a-z_]+)\s*\(([^;{]*?)\)\s*;", src, flags=re.S):
+        params = params.strip()
+        out[name] = 0 if params in ("", "void") else params.count(",") + 1
+    return out
+
+
+def test_binding_signatures_match_header():
+    # a ctypes prototype with the wrong number of parameters would pass the
+    # trailing ones (a size, the stream) mangled
+    L = mpa.lib()
+    arity = declared_arity()
+    assert set(arity) == set(mpa.EXPORTS)
+    for name, n in arity.items():
+        assert len(getattr(L, name).argtypes) == n, name
+
+
 def test_status_strings():
     for code in (0, -1, -2, -3, -4):
         assert mpa.status_string(code)
@@ -153,3 +173,27 @@ def test_plan_info_counts():
     sh32 = shape(num_seqs=5, total_q_tokens=74, max_blocks_per_seq=64, dtype=mpa.MPA_F32)
     assert mpa.plan_info(sh32, seq_lens, qsl).num_prefill_tiles == (-(-70 // 16) + 1) * 2
     assert info.decode_launches == 1
+
+
+def test_prefill_kv_splits_planned_for_short_chunks():
+    # one 256-token chunk on a 4096-token prefix, 32 q / 8 KV heads: 4 query
+    # tiles (64 tokens each at G = 4) x 8 KV heads = 32 workgroups, under the
+    # 256 target, so the 64-tile prefix is split 8 ways
+    sh = shape(num_seqs=1, num_q_heads=32, num_kv_heads=8, total_q_tokens=256, max_blocks_per_seq=272)
+    seq_lens, qsl = [4352], [0, 256]
+    info = mpa.plan_info(sh, seq_lens, qsl)
+    assert info.prefill_max_splits == 8
+    assert info.num_prefill_tiles == 4 * 8 * 8
+    n = mpa.workspace_size(sh, seq_lens, qsl)
+    assert n == 8 * 256 * 32 * (128 + 2) * 4
+    assert attention_rc(sh, seq_lens, qsl, ws=n - 1) == mpa.MPA_ERR_WORKSPACE
+    # enough query tiles already: no split
+    big = shape(num_seqs=1, num_q_heads=32, num_kv_heads=8, total_q_tokens=4096, max_blocks_per_seq=512)
+    assert mpa.plan_info(big, [8192], [0, 4096]).prefill_max_splits == 1
+    assert mpa.workspace_size(big, [8192], [0, 4096]) == 0
+    # a prefix shorter than 8 tiles is not split, nor is the f32 path
+    assert mpa.plan_info(sh, [256 + 300], qsl).prefill_max_splits == 1
+    sh32 = shape(num_seqs=1, num_q_heads=32, num_kv_heads=8, total_q_tokens=256, max_blocks_per_seq=272,
+                 dtype=mpa.MPA_F32)
+    assert mpa.plan_info(sh32, seq_lens, qsl).prefill_max_splits == 1
+    assert mpa.workspace_size(sh32, seq_lens, qsl) == 0
