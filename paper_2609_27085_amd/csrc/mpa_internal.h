@@ -14,7 +14,8 @@ constexpr int kMaxPlanSeqs = 256;     // sequences per launch (kernel-argument p
 constexpr int kMaxPrefillSeqs = 64;   // prefill chunks per launch (its plan carries more per chunk)
 constexpr int kPrefillSplitTarget = 256;  // prefill workgroups a launch should at least have
 constexpr int kPrefillMinSplitTiles = 8;  // smallest KV range of a prefill split, in 64-key tiles
-constexpr int kPrefillRows = 64;      // (token, head) rows per f32 prefill workgroup
+constexpr int kPrefillRows = 64;      // (token, head) rows per generic prefill workgroup
+constexpr int kFewKeys = 64;          // rows that see at most this many keys get the 16-bit P pass
 constexpr int kPrefillRowsMfma = 256; // (token, head) rows per bf16 prefill workgroup (8 waves)
 
 // Pointers and sizes common to the attention kernels.
@@ -98,6 +99,11 @@ hipError_t launch_decode(const AttnArgs& a, const DecodePlan& p, int n_items, in
 hipError_t launch_merge(const AttnArgs& a, const DecodePlan& p, int dtype, int head_dim, hipStream_t stream);
 hipError_t launch_prefill(const AttnArgs& a, const PrefillPlan& p, int n_tiles, int dtype, int head_dim,
                           hipStream_t stream);
+// The generic (16 rows per wave) prefill kernel for any dtype; in bf16 it
+// recomputes the rows of a chunk that see at most 64 keys, after the MFMA
+// kernel, with the probabilities carried to about 16 bits.
+hipError_t launch_prefill_generic(const AttnArgs& a, const PrefillPlan& p, int n_tiles, int dtype, int head_dim,
+                                  hipStream_t stream);
 // Combines the KV-split partial results of the plan's split chunks.
 hipError_t launch_prefill_merge(const AttnArgs& a, const PrefillPlan& p, int dtype, int head_dim,
                                 hipStream_t stream);

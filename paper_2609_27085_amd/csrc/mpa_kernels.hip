@@ -37,6 +37,14 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// acc + the two bf16 values packed in w (one v_dot2 against (1, 1)); the
+// products are exact and the sum is taken in f32
+__device__ inline float add_bf16_pair(unsigned w, float acc) {
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), one, acc, false);
+}
 
 constexpr float kLn2 = 0.69314718055994530942f;
 
@@ -110,14 +118,28 @@ struct Tr<0> {  // bf16
     for (int e = 0; e < 4; ++e) v[e] = e < nvalid ? v[e] : (short)0;
     return v;
   }
+  static constexpr bool kRoundsP = true;  // the PV product takes P in bf16
   static __device__ inline PFrag make_p(f32x4 p) {
     PFrag r;
 #pragma unroll
     for (int e = 0; e < 4; ++e) r[e] = bf16_bits(p[e]);
     return r;
   }
+  // p - hi rounded to bf16: hi + lo carries p to about 16 significant bits
+  static __device__ inline PFrag make_p_lo(f32x4 p, PFrag hi) {
+    PFrag r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r[e] = bf16_bits(p[e] - __uint_as_float((unsigned)(uint16_t)hi[e] << 16));
+    return r;
+  }
   static __device__ inline f32x4 pv(VFrag v, PFrag p, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(v, p, c, 0, 0, 0);
+  }
+  // acc + the probabilities exactly as the PV product consumes them (after
+  // rounding to bf16), so that the softmax denominator matches the numerator
+  static __device__ inline float psum(f32x4, PFrag pf, float acc) {
+    const u32x2 w = __builtin_bit_cast(u32x2, pf);
+    return add_bf16_pair(w[1], add_bf16_pair(w[0], acc));
   }
   static __device__ inline void store4(Elem* dst, f32x4 v) {
     s16x4 r;
@@ -148,7 +170,10 @@ struct Tr<1> {  // f32
     for (int e = 0; e < 4; ++e) v[e] = e < nvalid ? v[e] : 0.f;
     return v;
   }
+  static constexpr bool kRoundsP = false;
   static __device__ inline PFrag make_p(f32x4 p) { return p; }
+  static __device__ inline PFrag make_p_lo(f32x4, PFrag) { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+  static __device__ inline float psum(f32x4 p, PFrag, float acc) { return acc + ((p[0] + p[1]) + (p[2] + p[3])); }
   static __device__ inline f32x4 pv(VFrag v, PFrag p, f32x4 c) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) c = __builtin_amdgcn_mfma_f32_16x16x4f32(v[j], p[j], c, 0, 0, 0);
@@ -182,7 +207,7 @@ template <int DT, int D>
 struct RowState {
   f32x4 acc[D / 16];
   float m;  // reference maximum of the row's scaled scores (log2 units)
-  float l;  // this lane's part of the running sum of 2^(s*c - m)
+  float l;  // this lane's part of the running sum of 2^(s*c - m), as rounded for the PV product
 };
 
 template <int DT, int D>
@@ -219,7 +244,7 @@ __device__ inline void load_block(const AttnArgs& a, int blk, int g, BlockFrags<
 // causal limit; only then are scores masked and V rows of keys >= kend zeroed.
 template <int DT, int D>
 __device__ inline void consume_block(const AttnArgs& a, const typename Tr<DT>::Chunk* qf, const BlockFrags<DT, D>& f,
-                                     int kb, int kend, int limit, bool edge, RowState<DT, D>& st) {
+                                     int kb, int kend, int limit, bool edge, bool few_keys, RowState<DT, D>& st) {
   using T = Tr<DT>;
   constexpr int R = D / (4 * T::X);
   constexpr int MT = D / 16;
@@ -250,8 +275,24 @@ __device__ inline void consume_block(const AttnArgs& a, const typename Tr<DT>::C
   f32x4 p;
 #pragma unroll
   for (int i = 0; i < 4; ++i) p[i] = exp2_fast(s[i] - m);
-  st.l += (p[0] + p[1]) + (p[2] + p[3]);
   const auto pf = T::make_p(p);
+  st.l = T::psum(p, pf, st.l);
+  if constexpr (T::kRoundsP) {
+    if (few_keys) {
+      // rows of at most kFewKeys keys: few probabilities carry each output,
+      // so their bf16 rounding would not average out; the remainder p - hi
+      // goes through a second PV product
+      const auto plo = T::make_p_lo(p, pf);
+      st.l = T::psum(p, plo, st.l);
+      const int nvalid = edge ? kend - key0 : kBlock;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const auto v = T::keep_first(f.v[mt], nvalid);
+        st.acc[mt] = T::pv(v, plo, T::pv(v, pf, st.acc[mt]));
+      }
+      return;
+    }
+  }
   if (edge) {
     const int nvalid = kend - key0;
 #pragma unroll
@@ -276,6 +317,7 @@ __device__ inline void attend_blocks(const AttnArgs& a, const typename Tr<DT>::C
                                      const int32_t* bt, int g, int kb_begin, int kb_end, int kend,
                                      int limit, int min_limit, RowState<DT, D>& st, bool& poison) {
   const int lane = threadIdx.x & 63;
+  const bool few_keys = kend <= kFewKeys;  // every row sees at most kFewKeys keys
   for (int c0 = kb_begin; c0 < kb_end; c0 += 64) {
     const int c1 = min(kb_end, c0 + 64);
     const int ids = c0 + lane < c1 ? bt[c0 + lane] : 0;
@@ -293,11 +335,11 @@ __device__ inline void attend_blocks(const AttnArgs& a, const typename Tr<DT>::C
     for (int kb = c0; kb < c1; kb += 2) {
       load_block<DT, D>(a, block_id(kb + 1), g, fb);
       __builtin_amdgcn_sched_barrier(0);
-      consume_block<DT, D>(a, qf, fa, kb, kend, limit, is_edge(kb), st);
+      consume_block<DT, D>(a, qf, fa, kb, kend, limit, is_edge(kb), few_keys, st);
       if (kb + 1 >= c1) break;
       load_block<DT, D>(a, block_id(kb + 2), g, fa);
       __builtin_amdgcn_sched_barrier(0);
-      consume_block<DT, D>(a, qf, fb, kb + 1, kend, limit, is_edge(kb + 1), st);
+      consume_block<DT, D>(a, qf, fb, kb + 1, kend, limit, is_edge(kb + 1), few_keys, st);
     }
   }
 }
@@ -772,22 +814,25 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
         m_ref = m_new;
       }
       const float mc = m_ref * c;
+      // P^T in bf16; the row sum adds the rounded values the PV product
+      // uses (four independent partial sums, two probabilities per dot2).
+      // Rows that see at most 64 keys are recomputed afterwards by the
+      // generic prefill kernel, which keeps P to about 16 bits for them.
       bf16x8 pb[4];
-      float l4[4] = {0.f, 0.f, 0.f, 0.f};  // independent partial sums
+      float l4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float pv = exp2_fast(fmaf(st[t >> 1][8 * (t & 1) + e], c, -mc));
-          l4[e & 3] += pv;
-          pb[t][e] = (__bf16)pv;
-        }
+        for (int e = 0; e < 8; ++e) pb[t][e] = (__bf16)exp2_fast(fmaf(st[t >> 1][8 * (t & 1) + e], c, -mc));
+        const u32x4 w = __builtin_bit_cast(u32x4, pb[t]);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) l4[k] = add_bf16_pair(w[k], l4[k]);
       }
-      l += (l4[0] + l4[1]) + (l4[2] + l4[3]);
 #pragma unroll
       for (int t = 0; t < 4; ++t)
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[t][dt], pb[t], o[dt], 0, 0, 0);
+      l += (l4[0] + l4[1]) + (l4[2] + l4[3]);
     } else {
       copy_tile(kt + STAGES - 1, cblk);
       next_blk = tile_block(kt + STAGES);
@@ -945,6 +990,16 @@ hipError_t launch_prefill_mfma(const AttnArgs& a, const PrefillPlan& p, int n_ti
   return hipGetLastError();
 }
 
+// The generic prefill kernel for any dtype (the bf16 few-key pass).
+template <int DT, int D>
+struct PrefillGenericL {
+  static hipError_t run(const AttnArgs& a, const PrefillPlan& p, int n_tiles, hipStream_t stream) {
+    if (n_tiles == 0) return hipSuccess;
+    hipLaunchKernelGGL((prefill_kernel<DT, D>), dim3(n_tiles, a.hkv), dim3(64 * kWavesPerGroup), 0, stream, a, p);
+    return hipGetLastError();
+  }
+};
+
 template <int DT, int D>
 struct PrefillL {
   static hipError_t run(const AttnArgs& a, const PrefillPlan& p, int n_tiles, hipStream_t stream) {
@@ -1012,6 +1067,11 @@ hipError_t launch_prefill_merge(const AttnArgs& a, const PrefillPlan& p, int dty
 hipError_t launch_prefill(const AttnArgs& a, const PrefillPlan& p, int n_tiles, int dtype, int head_dim,
                           hipStream_t stream) {
   return dispatch<PrefillL>(dtype, head_dim, a, p, n_tiles, stream);
+}
+
+hipError_t launch_prefill_generic(const AttnArgs& a, const PrefillPlan& p, int n_tiles, int dtype, int head_dim,
+                                  hipStream_t stream) {
+  return dispatch<PrefillGenericL>(dtype, head_dim, a, p, n_tiles, stream);
 }
 
 }  // namespace mpa

@@ -4,7 +4,12 @@ Every case draws seeded inputs, runs mpa_kv_append then
 mpa_mixed_paged_attention on the GPU, and compares with the oracle run on the
 same arrays: the append bit for bit over the whole pool, attention outputs to
 max |err| <= 1e-2 and mean |err| <= 1e-3 for bf16 (1e-4 / 1e-5 for f32), and
-the log-sum-exp to 1e-4.
+the log-sum-exp to 2e-3 for bf16 (1e-4 for f32).
+
+The bf16 path rounds each probability to bf16 (relative error <= 2^-9) for
+the PV product and normalises by the sum of those rounded values, so its
+denominator, and with it the log-sum-exp, may differ from the exact one by a
+factor within 1 +- 2^-9: |d lse| <= -ln(1 - 2^-9) < 1.96e-3.
 """
 
 import dataclasses
@@ -15,14 +20,14 @@ import pytest
 
 import paper_2609_27085_amd as mpa
 from oracle import ref
-from workloads import HeadSpec, SeqSpec, make_batch
+from workloads import HeadSpec, SeqSpec, bf16_bits_from_f32, make_batch
 from workloads.configs import config_batch, config_specs
 from workloads.device import device_step, host_subbatch, tensor_to_raw, to_device
 
 pytestmark = pytest.mark.gpu
 
 TOL = {"bf16": (1e-2, 1e-3), "f32": (1e-4, 1e-5)}
-LSE_TOL = 1e-4
+LSE_TOL = {"bf16": 2e-3, "f32": 1e-4}
 
 
 @pytest.fixture(scope="module")
@@ -60,6 +65,10 @@ def as_f64(t):
     return t.float().cpu().numpy().astype(np.float64)
 
 
+def bf16_to_f32(bits):
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
 def oracle_for(b):
     return ref.attention_reference(b.q, b.k_cache, b.v_cache, b.k_new, b.v_new, b.block_tables, b.seq_lens,
                                    b.query_start_loc, b.scale, b.heads.num_kv_heads, b.heads.block_size, b.dtype)
@@ -86,7 +95,7 @@ def check_batch(b, what):
     rows = np.repeat(b.q_lens > 0, b.q_lens)
     assert_close(as_f64(out)[rows], o_ref[rows], b.dtype, what)
     lg = lse.cpu().numpy().astype(np.float64)[rows]
-    assert np.abs(lg - l_ref[rows]).max() <= LSE_TOL, f"{what}: lse err {np.abs(lg - l_ref[rows]).max():.3g}"
+    assert np.abs(lg - l_ref[rows]).max() <= LSE_TOL[b.dtype], f"{what}: lse err {np.abs(lg - l_ref[rows]).max():.3g}"
     return d, out, lse
 
 
@@ -139,6 +148,32 @@ def split_specs(rng):
     specs += [SeqSpec(int(c), 1) for c in rng.integers(1, 3000, size=5)]
     order = rng.permutation(len(specs))
     return [specs[i] for i in order]
+
+
+def few_key_specs(rng):
+    # rows that see a handful of keys: chunks without a cached prefix, short
+    # decode contexts, and a chunk on a short prefix (rows of 41..70 keys)
+    specs = [SeqSpec(64, 64) for _ in range(4)] + [SeqSpec(int(c), 1) for c in rng.integers(2, 9, size=16)]
+    specs += [SeqSpec(40 + 30, 30)]
+    order = rng.permutation(len(specs))
+    return [specs[i] for i in order]
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2, 3])
+def test_few_key_rows_at_rounding_floor(torch_gpu, seed):
+    """Rows that see few keys carry each output on a handful of
+    probabilities, whose bf16 rounding does not average out: such rows must
+    come out within 5e-4 of the exact result correctly rounded to bf16."""
+    rng = np.random.default_rng(700 + seed)
+    b = make_batch(few_key_specs(rng), HeadSpec(32, 8, 128), "bf16", rng)
+    d, out, _ = check_batch(b, f"few-key rows seed {seed}")
+    o_ref, _ = oracle_for(b)
+    keys = np.concatenate([b.seq_lens[s] - b.q_lens[s] + 1 + np.arange(b.q_lens[s]) for s in range(b.num_seqs)])
+    few = keys <= 48
+    exact = o_ref[few]
+    rounded = bf16_to_f32(bf16_bits_from_f32(exact.astype(np.float32))).astype(np.float64)
+    excess = np.abs(as_f64(out)[few] - exact) - np.abs(rounded - exact)
+    assert excess.max() <= 5e-4, f"few-key rows: {excess.max():.3g} above the bf16 rounding of the exact result"
 
 
 @pytest.mark.parametrize("heads", SPLIT_MIXES, ids=lambda h: f"hq{h[0]}_hkv{h[1]}_d{h[2]}")
@@ -366,6 +401,6 @@ def test_full_size_sampled(torch_gpu, name):
         o_ref, l_ref = oracle_rows(b, k, rows)
         g_rows = int(d.qsl_host[s]) + np.asarray(rows)
         assert_close(got[g_rows], o_ref, "bf16", f"{name} seq {s} rows {rows}")
-        assert np.abs(lg[g_rows] - l_ref).max() <= LSE_TOL
+        assert np.abs(lg[g_rows] - l_ref).max() <= LSE_TOL["bf16"]
     del d
     torch.cuda.empty_cache()
