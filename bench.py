@@ -15,6 +15,10 @@ before timing starts.  Prints one JSON line:
                  events between all phases (each event record costs ~4 us of
                  GPU time, so the timed steps carry only the two around the
                  dominant phase)
+  step_roofline  max(t_mem, t_mfma) / step time and (t_mem + t_mfma) / step time,
+                 t_mem and t_mfma being the step's algorithmic bytes at 8 TB/s and
+                 FLOPs at 2.5 PF
+  graph          (--graph) step time when the step is replayed from a HIP graph
   cpu_baseline   the CPU oracle, timed on a bounded sample of the same step
 
     python bench.py [--steps K] [--warmup W] [--config decode8b] [--seed 0]
@@ -195,6 +199,8 @@ def main(argv=None) -> int:
     ap.add_argument("--streams", type=int, default=1, choices=(1, 2),
                     help="2: the decode and prefill halves of the step run concurrently on two streams "
                          "(the library's mpa_decode_attention / mpa_prefill_attention); 1 (default): one after the other")
+    ap.add_argument("--graph", action="store_true",
+                    help="also capture one step into a HIP graph (torch.cuda.graph) and time its replays")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes 5 times (the reference kernel "
                          "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings) and exit")
@@ -228,8 +234,7 @@ def main(argv=None) -> int:
     ws = mpa.alloc_workspace(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.qsl_host, d.scale)
     out = torch.empty_like(d.q)
     lse = torch.empty(d.q.shape[:2], dtype=torch.float32, device=d.q.device)
-    stream = torch.cuda.current_stream()
-    side = torch.cuda.Stream() if args.streams == 2 else stream
+    side = torch.cuda.Stream() if args.streams == 2 else None
     has_dec = work["decode_rows"] > 0
     has_pre = work["prefill_chunks"] > 0
     two = args.streams == 2 and has_dec and has_pre
@@ -240,6 +245,7 @@ def main(argv=None) -> int:
         "end" -- to the event recorded there; marks absent from ev are not
         recorded."""
         ev = ev or {}
+        stream = torch.cuda.current_stream()  # the capture stream inside a graph capture
 
         def mark(name, s):
             if name in ev:
@@ -348,6 +354,31 @@ def main(argv=None) -> int:
         "step_hbm_gbs": round(total_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         "step_attention_tflops": round(total_flops / (ms_per_step * 1e-3) / 1e12, 3),
     }
+    # step roofline: the step's algorithmic bytes at 8 TB/s and FLOPs at the
+    # bf16 MFMA peak, against the measured step time
+    t_mem = total_bytes / (HBM_PEAK_GBS * 1e9)
+    t_mfma = work["prefill_flops"] / (MFMA_BF16_PEAK_TFLOPS * 1e12)
+    t_step = ms_per_step * 1e-3
+    line["step_roofline"] = {"t_mem_ms": round(t_mem * 1e3, 4), "t_mfma_ms": round(t_mfma * 1e3, 4),
+                             "max_frac": round(max(t_mem, t_mfma) / t_step, 4),
+                             "sum_frac": round((t_mem + t_mfma) / t_step, 4)}
+    if args.graph:
+        # the same step (no events) recorded once and replayed: every launch
+        # carries its plan as kernel arguments, so the graph is a fixed
+        # sequence of kernel nodes
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        for _ in range(max(1, args.warmup)):
+            graph.replay()
+        torch.cuda.synchronize()
+        g0 = time.perf_counter()
+        for _ in range(args.steps):
+            graph.replay()
+        torch.cuda.synchronize()
+        gwall = time.perf_counter() - g0
+        line["graph"] = {"ms_per_step": round(gwall * 1e3 / args.steps, 4),
+                         "value": round(work["query_tokens"] * args.steps / gwall, 1)}
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(d, args.cpu_seconds, args.seed)
     print(json.dumps(line), flush=True)
