@@ -18,6 +18,7 @@ before timing starts.  Prints one JSON line:
   step_roofline  max(t_mem, t_mfma) / step time and (t_mem + t_mfma) / step time,
                  t_mem and t_mfma being the step's algorithmic bytes at 8 TB/s and
                  FLOPs at 2.5 PF
+  model_ms       the library's step-time model (mpa_predict_step) for the batch
   graph          (--graph) step time when the step is replayed from a HIP graph
   cpu_baseline   the CPU oracle, timed on a bounded sample of the same step
 
@@ -362,6 +363,11 @@ def main(argv=None) -> int:
     line["step_roofline"] = {"t_mem_ms": round(t_mem * 1e3, 4), "t_mfma_ms": round(t_mfma * 1e3, 4),
                              "max_frac": round(max(t_mem, t_mfma) / t_step, 4),
                              "sum_frac": round((t_mem + t_mfma) / t_step, 4)}
+    # the library's step-time model (mpa_predict_step) for this batch
+    pred = mpa.predict_step(mpa.shape_of(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.scale),
+                            d.seq_lens_host, d.qsl_host)
+    line["model_ms"] = {"append": round(pred.append_us * 1e-3, 4), "decode": round(pred.decode_us * 1e-3, 4),
+                        "prefill": round(pred.prefill_us * 1e-3, 4), "step": round(pred.step_us * 1e-3, 4)}
     if args.graph:
         # the same step (no events) recorded once and replayed: every launch
         # carries its plan as kernel arguments, so the graph is a fixed

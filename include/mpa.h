@@ -207,6 +207,63 @@ typedef struct {
 int mpa_get_plan_info(const mpa_shape* shape, const int32_t* seq_lens_host,
                       const int32_t* query_start_loc_host, mpa_plan_info* info);
 
+/*
+ * Step-time model (host only; launches nothing).
+ *
+ * The paper has a decode node lend compute to spilled prefill under a lease
+ * whose compute credit is counted in units the backend can bound, such as
+ * token chunks (section 4.2), and admits a spill only when its predicted
+ * service time under that lease beats the default path (section 4.3); it
+ * stresses that the spare capacity beside a decode batch is nonlinear in the
+ * batch's shape (section 3.2).  mpa_predict_step gives that service time for
+ * this library: the device time of one step -- mpa_kv_append then
+ * mpa_mixed_paged_attention on one stream -- predicted from the library's
+ * own plan for the batch (decode splits, prefill query tiles, KV splits,
+ * launches) and a few measured rates:
+ *
+ *   append  = append_fixed_us + (bytes read and written) / append_gbs
+ *   decode  = per launch: decode_fixed_us + max(KV bytes / decode_gbs,
+ *             largest wave's KV bytes / decode_wave_gbs), plus merge_us per
+ *             launch when a row is split
+ *   prefill = per launch: the makespan of its workgroups, each taking
+ *             prefill_wg_us + prefill_tile_us per 64-key tile, dealt in
+ *             launch order to prefill_slots workgroup slots; plus
+ *             prefill_merge_us when a chunk is KV-split and prefill_fixup_us
+ *             when a chunk sits on a prefix shorter than 64 tokens
+ *
+ * Rates are in microseconds and GB/s (1e9 bytes/s).  mpa_default_rates
+ * fills in figures measured on one MI355X with bench.py.  Only bf16 caches
+ * are modelled: MPA_ERR_UNSUPPORTED for f32.
+ */
+typedef struct {
+  double append_fixed_us;
+  double append_gbs;
+  double decode_fixed_us;
+  double decode_gbs;
+  double decode_wave_gbs;
+  double merge_us;
+  double prefill_wg_us;
+  double prefill_tile_us;
+  double prefill_merge_us;
+  double prefill_fixup_us;
+  int32_t prefill_slots;
+} mpa_rates;
+
+typedef struct {
+  double append_us;
+  double decode_us;
+  double prefill_us;
+  double step_us; /* their sum: the three phases run one after the other */
+} mpa_step_time;
+
+void mpa_default_rates(mpa_rates* rates);
+
+/* rates may be NULL (the defaults).  Returns MPA_OK or an error code with
+ * *out untouched. */
+int mpa_predict_step(const mpa_shape* shape, const int32_t* seq_lens_host,
+                     const int32_t* query_start_loc_host, const mpa_rates* rates,
+                     mpa_step_time* out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -40,6 +40,8 @@ EXPORTS = (
     "mpa_get_plan_info",
     "mpa_decode_attention",
     "mpa_prefill_attention",
+    "mpa_default_rates",
+    "mpa_predict_step",
 )
 
 
@@ -80,6 +82,31 @@ class MpaPlanInfo(ctypes.Structure):
     ]
 
 
+class MpaRates(ctypes.Structure):
+    _fields_ = [
+        ("append_fixed_us", ctypes.c_double),
+        ("append_gbs", ctypes.c_double),
+        ("decode_fixed_us", ctypes.c_double),
+        ("decode_gbs", ctypes.c_double),
+        ("decode_wave_gbs", ctypes.c_double),
+        ("merge_us", ctypes.c_double),
+        ("prefill_wg_us", ctypes.c_double),
+        ("prefill_tile_us", ctypes.c_double),
+        ("prefill_merge_us", ctypes.c_double),
+        ("prefill_fixup_us", ctypes.c_double),
+        ("prefill_slots", ctypes.c_int32),
+    ]
+
+
+class MpaStepTime(ctypes.Structure):
+    _fields_ = [
+        ("append_us", ctypes.c_double),
+        ("decode_us", ctypes.c_double),
+        ("prefill_us", ctypes.c_double),
+        ("step_us", ctypes.c_double),
+    ]
+
+
 _lib = None
 _P = ctypes.c_void_p
 _I32P = ctypes.POINTER(ctypes.c_int32)
@@ -108,6 +135,10 @@ def lib() -> ctypes.CDLL:
         L.mpa_status_string.argtypes = [ctypes.c_int]
         L.mpa_get_plan_info.restype = ctypes.c_int
         L.mpa_get_plan_info.argtypes = [_SHP, _I32P, _I32P, ctypes.POINTER(MpaPlanInfo)]
+        L.mpa_default_rates.restype = None
+        L.mpa_default_rates.argtypes = [ctypes.POINTER(MpaRates)]
+        L.mpa_predict_step.restype = ctypes.c_int
+        L.mpa_predict_step.argtypes = [_SHP, _I32P, _I32P, ctypes.POINTER(MpaRates), ctypes.POINTER(MpaStepTime)]
         _lib = L
     return _lib
 
@@ -177,6 +208,25 @@ def plan_info(shape: MpaShape, seq_lens_host, qsl_host) -> MpaPlanInfo:
     if rc != MPA_OK:
         raise MpaError(rc, "mpa_get_plan_info")
     return info
+
+
+def default_rates() -> MpaRates:
+    """The library's measured MI355X rates for the step-time model."""
+    r = MpaRates()
+    lib().mpa_default_rates(ctypes.byref(r))
+    return r
+
+
+def predict_step(shape: MpaShape, seq_lens_host, qsl_host, rates: Optional[MpaRates] = None) -> MpaStepTime:
+    """Predicted device time (us) of kv_append + mixed attention for a batch
+    (mpa_predict_step); rates None means the library's defaults."""
+    sl, qs = _host_i32(seq_lens_host), _host_i32(qsl_host)
+    out = MpaStepTime()
+    rc = lib().mpa_predict_step(ctypes.byref(shape), _i32p(sl), _i32p(qs),
+                                ctypes.byref(rates) if rates is not None else None, ctypes.byref(out))
+    if rc != MPA_OK:
+        raise MpaError(rc, "mpa_predict_step")
+    return out
 
 
 def workspace_size(shape: MpaShape, seq_lens_host, qsl_host) -> int:

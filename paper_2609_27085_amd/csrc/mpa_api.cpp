@@ -8,6 +8,8 @@
 #include <string.h>
 
 #include <algorithm>
+#include <functional>
+#include <queue>
 #include <vector>
 
 #include "mpa.h"
@@ -211,6 +213,106 @@ int mpa_get_plan_info(const mpa_shape* shape, const int32_t* seq_lens_host, cons
   info->num_prefill_tiles = (int32_t)(tiles * shape->num_kv_heads);
   info->prefill_max_splits = max_split;
   info->decode_launches = (int32_t)((b.decode.size() + mpa::kMaxPlanSeqs - 1) / mpa::kMaxPlanSeqs);
+  return MPA_OK;
+}
+
+void mpa_default_rates(mpa_rates* r) {
+  if (!r) return;
+  // Least-squares fit (log error) to the phase times bench.py measured on
+  // one MI355X for decode8b, lent, agentic, budget0/256/1024/4096 and
+  // longctx (seed 0, each phase less the ~5 us of its event record); the
+  // merge, few-key and wave figures are single kernel times from rocprofv3
+  r->append_fixed_us = 6.5;
+  r->append_gbs = 1140.0;
+  r->decode_fixed_us = 2.0;
+  r->decode_gbs = 5600.0;
+  r->decode_wave_gbs = 4.8;
+  r->merge_us = 5.0;
+  r->prefill_wg_us = 18.0;
+  r->prefill_tile_us = 1.85;
+  r->prefill_merge_us = 5.0;
+  r->prefill_fixup_us = 8.0;
+  r->prefill_slots = 256;
+}
+
+int mpa_predict_step(const mpa_shape* shape, const int32_t* seq_lens_host, const int32_t* qsl_host,
+                     const mpa_rates* rates, mpa_step_time* out) {
+  if (!out) return MPA_ERR_INVALID;
+  Batch b;
+  int rc = check_batch(shape, seq_lens_host, qsl_host, nullptr, false, &b);
+  if (rc != MPA_OK) return rc;
+  if (shape->dtype != MPA_BF16) return MPA_ERR_UNSUPPORTED;
+  mpa_rates def;
+  mpa_default_rates(&def);
+  const mpa_rates& r = rates ? *rates : def;
+  if (!(r.append_gbs > 0) || !(r.decode_gbs > 0) || !(r.decode_wave_gbs > 0) || r.prefill_slots <= 0)
+    return MPA_ERR_INVALID;
+  const double elem = 2.0;  // bf16
+  const double row_bytes = (double)shape->num_kv_heads * shape->head_dim * elem;  // one token's K (or V)
+  mpa_step_time t = {0.0, 0.0, 0.0, 0.0};
+
+  // append: every new token's K and V read once and written once
+  if (shape->total_q_tokens > 0)
+    t.append_us = r.append_fixed_us + 4.0 * row_bytes * shape->total_q_tokens / (r.append_gbs * 1e3);
+
+  // decode, launch by launch as run_attention issues them
+  const int split = choose_split(shape, b, seq_lens_host);
+  const double head_bytes = 2.0 * shape->head_dim * elem;  // K + V of one token and KV head
+  for (size_t c0 = 0; c0 < b.decode.size(); c0 += mpa::kMaxPlanSeqs) {
+    const size_t c1 = std::min(b.decode.size(), c0 + mpa::kMaxPlanSeqs);
+    double bytes = 0.0, wave = 0.0;
+    bool split_any = false;
+    for (size_t k = c0; k < c1; ++k) {
+      const int L = seq_lens_host[b.decode[k]];
+      bytes += (double)L * head_bytes * shape->num_kv_heads;
+      wave = std::max(wave, (double)std::min(L, split) * head_bytes);
+      split_any |= L > split;
+    }
+    t.decode_us += r.decode_fixed_us + std::max(bytes / (r.decode_gbs * 1e3), wave / (r.decode_wave_gbs * 1e3));
+    if (split_any) t.decode_us += r.merge_us;
+  }
+
+  // prefill: each launch's workgroups, in launch order (longest query tiles
+  // first), on prefill_slots slots that take the next workgroup when free
+  const int qt = q_tile(shape);
+  const std::vector<PrefillSplit> psplit =
+      prefill_splits(shape, b, seq_lens_host, qsl_host, decode_items(shape, b, seq_lens_host, split));
+  bool few = false;
+  for (size_t c0 = 0; c0 < b.prefill.size(); c0 += mpa::kMaxPrefillSeqs) {
+    const size_t c1 = std::min(b.prefill.size(), c0 + mpa::kMaxPrefillSeqs);
+    std::vector<int> tiles;  // 64-key tiles of each work unit, in unit order
+    bool launch_split = false;
+    for (size_t k = c0; k < c1; ++k) {
+      const int s = b.prefill[k];
+      const int C = qsl_host[s + 1] - qsl_host[s];
+      const int P = seq_lens_host[s] - C;
+      const PrefillSplit& ps = psplit[k];
+      launch_split |= ps.nsplit > 1;
+      few |= P < mpa::kFewKeys;
+      for (int q = 0; q < (C + qt - 1) / qt; ++q) {
+        const int kend = P + std::min(q * qt + qt - 1, C - 1) + 1;
+        const int all = (kend + 63) / 64;
+        for (int x = 0; x < ps.nsplit; ++x)
+          tiles.push_back(x == ps.nsplit - 1 ? all - x * ps.tiles : ps.tiles);
+      }
+    }
+    std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
+    for (int i = 0; i < r.prefill_slots; ++i) free_at.push(0.0);
+    double makespan = 0.0;
+    // blockIdx order: the last unit first, each unit once per KV head
+    for (size_t u = tiles.size(); u-- > 0;)
+      for (int g = 0; g < shape->num_kv_heads; ++g) {
+        const double start = free_at.top();
+        free_at.pop();
+        const double end = start + r.prefill_wg_us + r.prefill_tile_us * tiles[u];
+        makespan = std::max(makespan, end);
+        free_at.push(end);
+      }
+    t.prefill_us += makespan + (launch_split ? r.prefill_merge_us : 0.0);
+  }
+  if (few) t.prefill_us += r.prefill_fixup_us;
+  t.step_us = t.append_us + t.decode_us + t.prefill_us;
+  *out = t;
   return MPA_OK;
 }
 

@@ -1,0 +1,132 @@
+"""The step-time model (mpa_predict_step): host-only checks of its
+arithmetic on hand-sized plans and of the shape dependence a lease needs.
+
+Prediction accuracy against measured steps is a GPU test
+(test_gpu_step_model.py).
+"""
+
+import math
+
+import numpy as np
+import pytest
+
+import paper_2609_27085_amd as mpa
+
+
+@pytest.fixture(scope="module")
+def L():
+    return mpa.lib()
+
+
+def shape(seq_lens, qsl, hq=32, hkv=8, d=128, dtype=mpa.MPA_BF16):
+    sl = np.asarray(seq_lens, np.int32)
+    return mpa.make_shape(num_seqs=len(sl), num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+                          num_blocks=int(sum((x + 15) // 16 for x in sl)) + 8,
+                          max_blocks_per_seq=int(max((x + 15) // 16 for x in sl)), total_q_tokens=int(qsl[-1]),
+                          scale=d ** -0.5, dtype=dtype)
+
+
+def batch(decode_ctx=(), chunks=()):
+    """decode contexts and (C, P) prefill chunks -> (seq_lens, qsl)"""
+    sl = list(decode_ctx) + [p + c for c, p in chunks]
+    ql = [1] * len(decode_ctx) + [c for c, _ in chunks]
+    return np.asarray(sl, np.int32), np.concatenate([[0], np.cumsum(ql)]).astype(np.int32)
+
+
+def predict(decode_ctx=(), chunks=(), rates=None, **kw):
+    sl, qsl = batch(decode_ctx, chunks)
+    return mpa.predict_step(shape(sl, qsl, **kw), sl, qsl, rates)
+
+
+def unit_rates(**over):
+    """rates that make each term easy to compute by hand"""
+    r = mpa.default_rates()
+    for k in ("append_fixed_us", "decode_fixed_us", "merge_us", "prefill_wg_us", "prefill_merge_us",
+              "prefill_fixup_us"):
+        setattr(r, k, 0.0)
+    r.append_gbs = r.decode_gbs = r.decode_wave_gbs = 1e12  # bandwidth terms ~0
+    r.prefill_tile_us = 1.0
+    for k, v in over.items():
+        setattr(r, k, v)
+    return r
+
+
+def test_default_rates_are_sane(L):
+    r = mpa.default_rates()
+    assert 1000 < r.decode_gbs <= 8000  # below the 8 TB/s datasheet peak
+    assert r.prefill_slots == 256
+    assert r.prefill_tile_us > 0 and r.append_gbs > 0 and r.decode_wave_gbs > 0
+
+
+def test_step_is_sum_of_phases(L):
+    t = predict([4000, 9000, 300], [(1024, 4096), (300, 0)])
+    assert min(t.append_us, t.decode_us, t.prefill_us) > 0
+    assert math.isclose(t.step_us, t.append_us + t.decode_us + t.prefill_us, rel_tol=1e-12)
+
+
+def test_f32_and_bad_rates_rejected(L):
+    sl, qsl = batch([100])
+    with pytest.raises(mpa.MpaError) as e:
+        mpa.predict_step(shape(sl, qsl, dtype=mpa.MPA_F32), sl, qsl)
+    assert e.value.status == mpa.MPA_ERR_UNSUPPORTED
+    r = mpa.default_rates()
+    r.prefill_slots = 0
+    with pytest.raises(mpa.MpaError):
+        mpa.predict_step(shape(sl, qsl), sl, qsl, r)
+
+
+def test_append_and_decode_bandwidth_terms(L):
+    # append: 4 * T * Hkv * d * 2 bytes over append_gbs (GB/s = 1e3 bytes/us)
+    r = unit_rates(append_gbs=1.0)
+    t = predict([50, 60, 70], rates=r)
+    assert math.isclose(t.append_us, 4 * 3 * 8 * 128 * 2 / 1e3, rel_tol=1e-12)
+    # decode: K+V bytes of every context token, or the largest wave alone
+    r = unit_rates(decode_gbs=2.0, decode_wave_gbs=1e12)
+    t = predict([100, 300], rates=r)
+    assert math.isclose(t.decode_us, 400 * 8 * 2 * 128 * 2 / 2e3, rel_tol=1e-12)
+    r = unit_rates(decode_gbs=1e12, decode_wave_gbs=1.0)
+    t = predict([100, 60], rates=r)
+    assert math.isclose(t.decode_us, 100 * 2 * 128 * 2 / 1e3, rel_tol=1e-12)
+
+
+def test_prefill_makespan_by_hand(L):
+    # one KV head, G = 4: query tiles of 256 / 4 = 64 tokens; 1 us per tile
+    kw = dict(hq=4, hkv=1)
+    # C = 64 on P = 128: one unit of ceil(192 / 64) = 3 tiles
+    assert predict(chunks=[(64, 128)], rates=unit_rates(), **kw).prefill_us == pytest.approx(3.0)
+    # C = 128 on P = 128: units of 3 and 4 tiles; one slot runs them back to back
+    assert predict(chunks=[(128, 128)], rates=unit_rates(prefill_slots=1), **kw).prefill_us == pytest.approx(7.0)
+    # ... two slots run them side by side
+    assert predict(chunks=[(128, 128)], rates=unit_rates(prefill_slots=2), **kw).prefill_us == pytest.approx(4.0)
+    # two KV heads double the units: 4 workgroups (4, 4, 3, 3 tiles, longest
+    # first) on 3 slots -> 4 | 4 | 3 + 3
+    kw2 = dict(hq=8, hkv=2)
+    assert predict(chunks=[(128, 128)], rates=unit_rates(prefill_slots=3), **kw2).prefill_us == pytest.approx(6.0)
+    # fixed workgroup cost and the few-key pass (prefix under 64 tokens)
+    r = unit_rates(prefill_wg_us=10.0, prefill_fixup_us=100.0)
+    assert predict(chunks=[(64, 128)], rates=r, **kw).prefill_us == pytest.approx(13.0)
+    assert predict(chunks=[(64, 0)], rates=r, **kw).prefill_us == pytest.approx(111.0)
+
+
+def test_short_chunk_on_long_prefix_is_split(L):
+    # 256 tokens on a 4352-token prefix: 4 query tiles x 8 heads = 32 units,
+    # so the library splits the prefix 8 ways (see the planner test); the
+    # model follows the split plan and adds the merge
+    r = unit_rates(prefill_merge_us=1000.0)
+    t = predict(chunks=[(256, 4352)], rates=r)
+    assert 1000.0 < t.prefill_us < 1000.0 + (4352 + 256) / 64
+
+
+def test_shape_dependence(L):
+    """What the lease needs: prefill service grows with the chunk and with
+    the cached prefix it attends to, while decode cost follows the KV bytes
+    read, not the number of rows."""
+    base = predict([6000] * 64)
+    more_chunk = [predict([6000] * 64, [(c, 4096)]).prefill_us for c in (256, 1024, 4096)]
+    more_prefix = [predict([6000] * 64, [(1024, p)]).prefill_us for p in (0, 8192, 65536)]
+    assert base.prefill_us == 0.0
+    assert more_chunk == sorted(more_chunk) and more_prefix == sorted(more_prefix)
+    # decode: same total KV bytes in different shapes cost about the same
+    a = predict([8192] * 32).decode_us
+    b = predict([2048] * 128).decode_us
+    assert abs(a - b) / a < 0.05
