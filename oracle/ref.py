@@ -25,6 +25,11 @@ softmax attention with these readings of what the paper leaves unsaid:
   sequence's keys from the pool as it was *before* the append, plus this
   step's ``k_new`` / ``v_new`` rows for positions ``P .. L - 1``.
 
+The step may also rotate the new queries and keys by their positions before
+the append (the rotary embedding, ``rope_reference``); the paper describes
+neither its models' position encoding nor such a kernel, so that function is
+the standard rotate-half definition with the rounding spelled out.
+
 Cache layout read here (the library header's definition), with
 ``X = 16 / element_bytes``: K element (block b, head h, slot t, dim i) is at
 ``[b][h][i // X][t][i % X]``; V element (b, h, t, i) is at ``[b][h][i][t]``.
@@ -194,3 +199,57 @@ def append_reference(k_cache, v_cache, k_new, v_new, block_tables, seq_lens, que
         k5[blk, :, :, slot, :] = k_new[t0:t1].reshape(t1 - t0, hkv, d // x, x)
         v4[blk, :, :, slot] = v_new[t0:t1]
     return kc, vc
+
+
+def round_bf16(x32: np.ndarray) -> np.ndarray:
+    """float32 -> bf16 bit patterns, round to nearest, ties to even; NaN stays
+    a (quiet) NaN."""
+    x32 = np.ascontiguousarray(x32, dtype=np.float32)
+    u = x32.view(np.uint32).astype(np.uint64)
+    r = ((u + np.uint64(0x7FFF) + ((u >> np.uint64(16)) & np.uint64(1))) >> np.uint64(16)).astype(np.uint16)
+    nan = np.isnan(x32)
+    r[nan] = ((x32.view(np.uint32)[nan] >> np.uint32(16)) | np.uint32(0x40)).astype(np.uint16)
+    return r
+
+
+def rope_reference(x_raw, positions, cos_sin, rope_dim, dtype):
+    """Rotary position embedding of rows ``x [T, H, d]`` (raw storage), row t
+    at position ``positions[t]``, in the rotate-half form over the first
+    ``rope_dim`` dimensions.
+
+    The paper describes neither its models' position encoding nor a fused
+    kernel; this is the standard rotary embedding, applied where the step
+    writes new keys (and to the queries).  With R = rope_dim, for j < R/2 and
+    the caller's angle table ``cos_sin[p, j] = (cos, sin)``:
+
+        y[j]       = x[j] * cos - x[j + R/2] * sin
+        y[j + R/2] = x[j + R/2] * cos + x[j] * sin
+
+    and ``y[i] = x[i]`` for i >= R.  Every product and the sum are rounded to
+    float32 (no fused multiply-add) and the result is rounded to the storage
+    type (bf16: nearest even), so that the float32 rounding that decides
+    each stored code is the same on both sides.  Returns raw storage."""
+    x = decode_raw(x_raw, dtype).astype(np.float32)  # exact: inputs are bf16 or f32
+    t, h, d = x.shape
+    half = rope_dim // 2
+    cs = np.asarray(cos_sin, dtype=np.float32)[np.asarray(positions)]  # [T, R/2, 2]
+    c = cs[:, None, :, 0]
+    s = cs[:, None, :, 1]
+    x1, x2 = x[:, :, :half], x[:, :, half:rope_dim]
+    y = x.copy()
+    with np.errstate(over="ignore", invalid="ignore"):
+        y[:, :, :half] = (x1 * c).astype(np.float32) - (x2 * s).astype(np.float32)
+        y[:, :, half:rope_dim] = (x2 * c).astype(np.float32) + (x1 * s).astype(np.float32)
+    if dtype == "bf16":
+        return round_bf16(y)
+    return y
+
+
+def new_token_positions(seq_lens, query_start_loc):
+    """Position P_s + i of every new token (row of q / k_new)."""
+    qsl = np.asarray(query_start_loc)
+    pos = np.zeros(int(qsl[-1]), dtype=np.int64)
+    for s in range(len(seq_lens)):
+        t0, t1 = int(qsl[s]), int(qsl[s + 1])
+        pos[t0:t1] = int(seq_lens[s]) - (t1 - t0) + np.arange(t1 - t0)
+    return pos

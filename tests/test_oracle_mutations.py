@@ -55,7 +55,31 @@ def _transposed_gather(k_cache, v_cache, block_row, n_tokens, num_kv_heads, head
     return k[:n_tokens], v[:n_tokens]
 
 
+def _rope_interleaved(x_raw, positions, cos_sin, rope_dim, dtype):
+    # wrong: rotates adjacent pairs (2j, 2j+1) instead of (j, j + R/2)
+    x = ref.decode_raw(x_raw, dtype).astype(np.float32)
+    cs = np.asarray(cos_sin, np.float32)[np.asarray(positions)]
+    c, s = cs[:, None, :, 0], cs[:, None, :, 1]
+    y = x.copy()
+    a, b = x[:, :, 0:rope_dim:2], x[:, :, 1:rope_dim:2]
+    y[:, :, 0:rope_dim:2] = a * c - b * s
+    y[:, :, 1:rope_dim:2] = b * c + a * s
+    return ref.round_bf16(y) if dtype == "bf16" else y
+
+
+def _rope_sign(x_raw, positions, cos_sin, rope_dim, dtype):
+    # wrong: rotates the other way
+    cs = np.asarray(cos_sin, np.float32).copy()
+    cs[..., 1] = -cs[..., 1]
+    return _good_rope(x_raw, positions, cs, rope_dim, dtype)
+
+
+_good_rope = ref.rope_reference
+
+
 MUTANTS = {
+    "rope_interleaved_pairs": ("rope_reference", _rope_interleaved),
+    "rope_reversed": ("rope_reference", _rope_sign),
     "top_left_causal": ("sequence_attention", _seq_attn_factory(
         visible_fn=lambda keys, rows, prefix: keys[None] <= rows[:, None])),
     "exclusive_diagonal": ("sequence_attention", _seq_attn_factory(
@@ -73,6 +97,8 @@ PIN_TESTS = [
     lambda: pins.test_brute_force("bf16", 1),
     lambda: pins.test_block_size_invariance_and_sdpa("f32"),
     lambda: pins.test_zero_query_gives_running_mean(),
+    lambda: pins.test_rope_hand_worked(),
+    lambda: pins.test_rope_zero_and_quarter_turn("f32"),
 ]
 
 

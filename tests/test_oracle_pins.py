@@ -417,3 +417,68 @@ def test_bf16_decode_and_rounding():
     x = np.random.default_rng(12).standard_normal(100000, dtype=np.float32) * 100
     tb = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
     assert np.array_equal(bf16_bits_from_f32(x), tb)
+
+
+# ----------------------------------------------------------------------------
+# rotary position embedding (the append step's optional rotation)
+
+
+def theta_table(max_pos, rope_dim, base=10000.0):
+    """The standard rotary angle table, cos/sin of p * base^(-2j/R), in float64
+    then stored as float32 (what a caller hands the library)."""
+    j = np.arange(rope_dim // 2)
+    ang = np.arange(max_pos)[:, None] * base ** (-2.0 * j / rope_dim)[None, :]
+    return np.stack([np.cos(ang), np.sin(ang)], axis=-1).astype(np.float32)
+
+
+def test_rope_hand_worked():
+    # d = R = 8, one angle with cos 1/2 and sin 1/4 (both exact in binary):
+    # pairs (j, j+4): y_j = x_j/2 - x_{j+4}/4, y_{j+4} = x_{j+4}/2 + x_j/4
+    x = np.arange(1, 9, dtype=np.float32).reshape(1, 1, 8)
+    cs = np.tile(np.array([0.5, 0.25], np.float32), (1, 4, 1))
+    y = ref.rope_reference(x, [0], cs, 8, "f32")
+    assert y.ravel().tolist() == [-0.75, -0.5, -0.25, 0.0, 2.75, 3.5, 4.25, 5.0]
+    # rope_dim 4 of d 8: pairs (0, 2), (1, 3); dims 4..7 pass through
+    y = ref.rope_reference(x, [0], cs[:, :2], 4, "f32")
+    assert y.ravel().tolist() == [1 * .5 - 3 * .25, 2 * .5 - 4 * .25, 3 * .5 + 1 * .25, 4 * .5 + 2 * .25,
+                                  5, 6, 7, 8]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_rope_zero_and_quarter_turn(dtype):
+    rng = np.random.default_rng(40)
+    x32 = rng.standard_normal((5, 3, 64)).astype(np.float32)
+    raw = bf16_bits_from_f32(x32) if dtype == "bf16" else x32
+    zero = np.tile(np.array([1.0, 0.0], np.float32), (1, 32, 1))
+    assert np.array_equal(ref.rope_reference(raw, [0] * 5, zero, 64, dtype), raw)
+    quarter = np.tile(np.array([0.0, 1.0], np.float32), (1, 32, 1))
+    y = ref.decode_raw(ref.rope_reference(raw, [0] * 5, quarter, 64, dtype), dtype)
+    x = ref.decode_raw(raw, dtype)
+    assert np.array_equal(y[..., :32], -x[..., 32:]) and np.array_equal(y[..., 32:], x[..., :32])
+
+
+def test_rope_preserves_pair_norms_and_relative_position():
+    rng = np.random.default_rng(41)
+    d, rd = 128, 96
+    tab = theta_table(4096, rd)
+    q = rng.standard_normal((1, 1, d)).astype(np.float32)
+    k = rng.standard_normal((1, 1, d)).astype(np.float32)
+    yq = ref.rope_reference(q, [777], tab, rd, "f32").astype(np.float64)
+    # each rotated pair keeps its length (up to float32 rounding); dims >= R pass
+    n0 = q[0, 0, :rd // 2] ** 2 + q[0, 0, rd // 2:rd] ** 2
+    n1 = yq[0, 0, :rd // 2] ** 2 + yq[0, 0, rd // 2:rd] ** 2
+    assert np.allclose(n1, n0, rtol=1e-6) and np.array_equal(yq[0, 0, rd:], q[0, 0, rd:])
+    # q.k after rotation depends on the position difference only
+    dots = [float(ref.rope_reference(q, [p], tab, rd, "f32").astype(np.float64).ravel()
+                  @ ref.rope_reference(k, [p - 300], tab, rd, "f32").astype(np.float64).ravel())
+            for p in (300, 1000, 3000)]
+    assert np.allclose(dots, dots[0], rtol=1e-5, atol=1e-5)
+    # ... and does change with it
+    other = float(ref.rope_reference(q, [1000], tab, rd, "f32").astype(np.float64).ravel()
+                  @ ref.rope_reference(k, [1000 - 301], tab, rd, "f32").astype(np.float64).ravel())
+    assert abs(other - dots[0]) > 1e-3
+
+
+def test_rope_positions_of_new_tokens():
+    pos = ref.new_token_positions([5, 9, 3], [0, 1, 4, 4])
+    assert pos.tolist() == [4, 6, 7, 8]
