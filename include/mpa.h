@@ -122,6 +122,36 @@ int mpa_kv_append(const mpa_shape* shape, const void* k_new, const void* v_new, 
                   void* stream);
 
 /*
+ * mpa_kv_append with the rotary position embedding applied on the way:
+ * every new token's query row (all Hq heads, in place) and key row are
+ * rotated by the token's position p = seq_lens[s] - q_len(s) + i before the
+ * key is written to the cache; values are appended unchanged.  The paper
+ * describes neither its models' position encoding nor such a kernel; this
+ * is the standard rotary embedding in the rotate-half form, fused into the
+ * step that writes the cache.  With R = rope_dim and, for j < R/2,
+ * (c, s) = rope_cos_sin[p][j]:
+ *   y[j]       = x[j] * c - x[j + R/2] * s
+ *   y[j + R/2] = x[j + R/2] * c + x[j] * s
+ * and y[i] = x[i] for i >= R (partial rotary when R < d).  Each product and
+ * each sum is rounded to float32 (no fused multiply-add), the result to the
+ * cache's element type (bf16: nearest even).
+ *
+ * q                 device [T][Hq][d], rotated in place
+ * rope_cos_sin      device float32 [rope_max_pos][R/2][2] (cos, sin), e.g.
+ *                   cos/sin of p * base^(-2j/R); any table (scaled variants
+ *                   included) may be passed
+ * rope_dim          R: a multiple of 16, at most head_dim
+ * rope_max_pos      rows of the table; every position must be below it
+ *                   (checked against seq_lens_host)
+ * Other arguments, ownership and errors as for mpa_kv_append.
+ */
+int mpa_kv_append_rope(const mpa_shape* shape, void* q, const void* k_new, const void* v_new, void* k_cache,
+                       void* v_cache, const int32_t* block_tables, const int32_t* seq_lens,
+                       const int32_t* query_start_loc, const int32_t* seq_lens_host,
+                       const int32_t* query_start_loc_host, const int32_t* block_tables_host,
+                       const float* rope_cos_sin, int32_t rope_dim, int32_t rope_max_pos, void* stream);
+
+/*
  * Bytes of device workspace that mpa_mixed_paged_attention needs for this
  * batch: the split-K partial results of long decode rows, and of prefill
  * chunks whose cached prefix is split across workgroups (short bf16 chunks

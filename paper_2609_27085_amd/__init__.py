@@ -41,6 +41,7 @@ EXPORTS = (
     "mpa_decode_attention",
     "mpa_prefill_attention",
     "mpa_default_rates",
+    "mpa_kv_append_rope",
     "mpa_predict_step",
 )
 
@@ -122,6 +123,9 @@ def lib() -> ctypes.CDLL:
         L = ctypes.CDLL(LIB_PATH)
         L.mpa_kv_append.restype = ctypes.c_int
         L.mpa_kv_append.argtypes = [_SHP, _P, _P, _P, _P, _P, _P, _P, _I32P, _I32P, _I32P, _P]
+        L.mpa_kv_append_rope.restype = ctypes.c_int
+        L.mpa_kv_append_rope.argtypes = [_SHP, _P, _P, _P, _P, _P, _P, _P, _P, _I32P, _I32P, _I32P, _P,
+                                         ctypes.c_int32, ctypes.c_int32, _P]
         L.mpa_mixed_paged_attention.restype = ctypes.c_int
         L.mpa_mixed_paged_attention.argtypes = [
             _SHP, _P, _P, _P, _P, _P, _P, _I32P, _I32P, _I32P, _P, _P, _P, ctypes.c_size_t, _P]
@@ -256,6 +260,26 @@ def kv_append(k_new, v_new, k_cache, v_cache, block_tables, seq_lens, query_star
         _ptr(seq_lens), _ptr(query_start_loc), _i32p(sl), _i32p(qs), _i32p(bth), _stream(stream))
     if rc != MPA_OK:
         raise MpaError(rc, "mpa_kv_append")
+
+
+def kv_append_rope(q, k_new, v_new, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host,
+                   qsl_host, cos_sin, rope_dim=None, block_tables_host=None, stream=None) -> None:
+    """mpa_kv_append_rope: q [T, Hq, d] rotated in place, k_new rotated into
+    the cache, v_new appended; cos_sin is a float32 device tensor
+    [max_pos, R/2, 2] (rope_dim R defaults to 2 * cos_sin.shape[1])."""
+    t, hkv, d = k_new.shape
+    hq = q.shape[1]
+    if rope_dim is None:
+        rope_dim = 2 * int(cos_sin.shape[1])
+    sl, qs = _host_i32(seq_lens_host), _host_i32(qsl_host)
+    bth = None if block_tables_host is None else _host_i32(block_tables_host)
+    shape = make_shape(len(sl), hq, hkv, d, k_cache.shape[0], block_tables.shape[1], t, 1.0, _dtype_code(k_new))
+    rc = lib().mpa_kv_append_rope(
+        ctypes.byref(shape), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(block_tables),
+        _ptr(seq_lens), _ptr(query_start_loc), _i32p(sl), _i32p(qs), _i32p(bth), _ptr(cos_sin), int(rope_dim),
+        int(cos_sin.shape[0]), _stream(stream))
+    if rc != MPA_OK:
+        raise MpaError(rc, "mpa_kv_append_rope")
 
 
 def _attention(which, q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host, out,

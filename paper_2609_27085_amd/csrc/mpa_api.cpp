@@ -174,6 +174,56 @@ long prefill_items(const std::vector<PrefillSplit>& sp, const Batch& b, const in
   return n;
 }
 
+// The append launches (plain, or with the rotary embedding when rope is
+// given): one wave per new token, up to kMaxPlanSeqs sequences per launch.
+int run_append(const mpa_shape* shape, const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+               const int32_t* block_tables, const int32_t* seq_lens, const int32_t* query_start_loc,
+               const int32_t* seq_lens_host, const int32_t* query_start_loc_host, const int32_t* block_tables_host,
+               const mpa::RopeArgs* rope, void* stream) {
+  Batch b;
+  int rc = check_batch(shape, seq_lens_host, query_start_loc_host, block_tables_host, true, &b);
+  if (rc != MPA_OK) return rc;
+  if (shape->total_q_tokens == 0) return MPA_OK;
+  if (!k_new || !v_new || !k_cache || !v_cache || !block_tables || !seq_lens || !query_start_loc)
+    return MPA_ERR_INVALID;
+  mpa::AppendArgs a;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.block_tables = block_tables;
+  a.hkv = shape->num_kv_heads;
+  a.mb = shape->max_blocks_per_seq;
+  a.nb = shape->num_blocks;
+  (void)seq_lens;
+  (void)query_start_loc;
+  std::vector<int> seqs(b.decode);
+  seqs.insert(seqs.end(), b.prefill.begin(), b.prefill.end());
+  clear_stale_hip_error();
+  for (size_t c0 = 0; c0 < seqs.size(); c0 += mpa::kMaxPlanSeqs) {
+    mpa::AppendPlan p;
+    memset(&p, 0, sizeof(p));
+    const size_t c1 = std::min(seqs.size(), c0 + mpa::kMaxPlanSeqs);
+    p.n_seqs = (int32_t)(c1 - c0);
+    int acc = 0;
+    for (size_t k = c0; k < c1; ++k) {
+      const int s = seqs[k];
+      const int ql = query_start_loc_host[s + 1] - query_start_loc_host[s];
+      p.seq[k - c0] = s;
+      p.row0[k - c0] = query_start_loc_host[s];
+      p.pos0[k - c0] = seq_lens_host[s] - ql;
+      p.tok_start[k - c0] = acc;
+      acc += ql;
+    }
+    p.tok_start[c1 - c0] = acc;
+    p.unit = acc == (int)(c1 - c0) ? 1 : 0;
+    hipError_t e = rope ? mpa::launch_rope_append(a, p, *rope, shape->dtype, shape->head_dim, (hipStream_t)stream)
+                        : mpa::launch_append(a, p, shape->dtype, shape->head_dim, (hipStream_t)stream);
+    if (e != hipSuccess) return MPA_ERR_HIP;
+  }
+  return MPA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -332,47 +382,29 @@ int mpa_kv_append(const mpa_shape* shape, const void* k_new, const void* v_new, 
                   const int32_t* block_tables, const int32_t* seq_lens, const int32_t* query_start_loc,
                   const int32_t* seq_lens_host, const int32_t* query_start_loc_host,
                   const int32_t* block_tables_host, void* stream) {
-  Batch b;
-  int rc = check_batch(shape, seq_lens_host, query_start_loc_host, block_tables_host, true, &b);
-  if (rc != MPA_OK) return rc;
-  if (shape->total_q_tokens == 0) return MPA_OK;
-  if (!k_new || !v_new || !k_cache || !v_cache || !block_tables || !seq_lens || !query_start_loc)
+  return run_append(shape, k_new, v_new, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host,
+                    query_start_loc_host, block_tables_host, nullptr, stream);
+}
+
+int mpa_kv_append_rope(const mpa_shape* shape, void* q, const void* k_new, const void* v_new, void* k_cache,
+                       void* v_cache, const int32_t* block_tables, const int32_t* seq_lens,
+                       const int32_t* query_start_loc, const int32_t* seq_lens_host,
+                       const int32_t* query_start_loc_host, const int32_t* block_tables_host,
+                       const float* rope_cos_sin, int32_t rope_dim, int32_t rope_max_pos, void* stream) {
+  if (!shape) return MPA_ERR_INVALID;
+  if (rope_dim <= 0 || rope_dim % 16 != 0 || rope_dim > shape->head_dim || rope_max_pos <= 0)
     return MPA_ERR_INVALID;
-  mpa::AppendArgs a;
-  a.k_new = k_new;
-  a.v_new = v_new;
-  a.k_cache = k_cache;
-  a.v_cache = v_cache;
-  a.block_tables = block_tables;
-  a.hkv = shape->num_kv_heads;
-  a.mb = shape->max_blocks_per_seq;
-  a.nb = shape->num_blocks;
-  (void)seq_lens;
-  (void)query_start_loc;
-  std::vector<int> seqs(b.decode);
-  seqs.insert(seqs.end(), b.prefill.begin(), b.prefill.end());
-  clear_stale_hip_error();
-  for (size_t c0 = 0; c0 < seqs.size(); c0 += mpa::kMaxPlanSeqs) {
-    mpa::AppendPlan p;
-    memset(&p, 0, sizeof(p));
-    const size_t c1 = std::min(seqs.size(), c0 + mpa::kMaxPlanSeqs);
-    p.n_seqs = (int32_t)(c1 - c0);
-    int acc = 0;
-    for (size_t k = c0; k < c1; ++k) {
-      const int s = seqs[k];
-      const int ql = query_start_loc_host[s + 1] - query_start_loc_host[s];
-      p.seq[k - c0] = s;
-      p.row0[k - c0] = query_start_loc_host[s];
-      p.pos0[k - c0] = seq_lens_host[s] - ql;
-      p.tok_start[k - c0] = acc;
-      acc += ql;
-    }
-    p.tok_start[c1 - c0] = acc;
-    p.unit = acc == (int)(c1 - c0) ? 1 : 0;
-    hipError_t e = mpa::launch_append(a, p, shape->dtype, shape->head_dim, (hipStream_t)stream);
-    if (e != hipSuccess) return MPA_ERR_HIP;
-  }
-  return MPA_OK;
+  if (shape->total_q_tokens > 0 && (!q || !rope_cos_sin)) return MPA_ERR_INVALID;
+  if (seq_lens_host && shape->num_seqs > 0)
+    for (int s = 0; s < shape->num_seqs; ++s)
+      if (seq_lens_host[s] > rope_max_pos) return MPA_ERR_INVALID;  // a position past the table
+  mpa::RopeArgs r;
+  r.q = q;
+  r.cos_sin = rope_cos_sin;
+  r.hq = shape->num_q_heads;
+  r.half = rope_dim / 2;
+  return run_append(shape, k_new, v_new, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host,
+                    query_start_loc_host, block_tables_host, &r, stream);
 }
 
 }  // extern "C"

@@ -76,6 +76,14 @@ struct AppendArgs {
   int32_t hkv, mb, nb;
 };
 
+// The rotary embedding applied by the rope append: query rows (in place,
+// [T][Hq][d]) and the angle table cos_sin[pos][half][2] (cos, sin).
+struct RopeArgs {
+  void* q;
+  const float* cos_sin;
+  int32_t hq, half;
+};
+
 // Append work for up to kMaxPlanSeqs sequences: token k of this launch is new
 // token (k - tok_start[j]) of sequence seq[j]; that token is query row
 // row0[j] + (k - tok_start[j]) at position pos0[j] + (k - tok_start[j]).
@@ -92,6 +100,8 @@ struct AppendPlan {
 // Launchers (mpa_kernels.hip).  dtype: 0 = bf16, 1 = f32.  Return the HIP
 // error of the launch.
 hipError_t launch_append(const AppendArgs& a, const AppendPlan& p, int dtype, int head_dim, hipStream_t stream);
+hipError_t launch_rope_append(const AppendArgs& a, const AppendPlan& p, const RopeArgs& r, int dtype, int head_dim,
+                              hipStream_t stream);
 // Decode waves the current device holds at once (2048 without a device).
 int decode_wave_slots(int dtype, int head_dim);
 hipError_t launch_decode(const AttnArgs& a, const DecodePlan& p, int n_items, int dtype, int head_dim,

@@ -148,6 +148,17 @@ struct Tr<0> {  // bf16
     *reinterpret_cast<u32x2*>(dst) = __builtin_bit_cast(u32x2, r);
   }
   static __device__ inline void store1(Elem* dst, float v) { *dst = (uint16_t)bf16_bits(v); }
+  static __device__ inline void unpack(u32x4 w, float (&f)[X]) {
+#pragma unroll
+    for (int e = 0; e < X; ++e) f[e] = __uint_as_float(((w[e / 2] >> (16 * (e & 1))) & 0xFFFFu) << 16);
+  }
+  static __device__ inline u32x4 pack(const float (&f)[X]) {
+    u32x4 w;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      w[i] = (unsigned)(uint16_t)bf16_bits(f[2 * i]) | ((unsigned)(uint16_t)bf16_bits(f[2 * i + 1]) << 16);
+    return w;
+  }
 };
 
 template <>
@@ -181,6 +192,16 @@ struct Tr<1> {  // f32
   }
   static __device__ inline void store4(Elem* dst, f32x4 v) { *reinterpret_cast<f32x4*>(dst) = v; }
   static __device__ inline void store1(Elem* dst, float v) { *dst = v; }
+  static __device__ inline void unpack(u32x4 w, float (&f)[X]) {
+#pragma unroll
+    for (int e = 0; e < X; ++e) f[e] = __uint_as_float(w[e]);
+  }
+  static __device__ inline u32x4 pack(const float (&f)[X]) {
+    u32x4 w;
+#pragma unroll
+    for (int e = 0; e < X; ++e) w[e] = __float_as_uint(f[e]);
+    return w;
+  }
 };
 
 // Largest j in [0, n) with starts[j] <= x (starts non-decreasing, starts[0] <= x).
@@ -927,6 +948,85 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a, AppendPlan p)
   }
 }
 
+// Rotary embedding of 16-byte chunk c of one head row (rotate-half form):
+// element i < half pairs with i + half; with the position's angle row cs
+// (cos, sin interleaved per pair), y_i = x_i cos - x_{i+half} sin and
+// y_{i+half} = x_{i+half} cos + x_i sin, and elements >= 2*half are copied.
+// half is a multiple of the chunk's element count.  Each product and each
+// sum is rounded to f32 (no fused multiply-add), then the result to the
+// storage type.
+template <int DT>
+__device__ inline u32x4 rope_chunk(const typename Tr<DT>::Elem* row, int c, int half, const float* cs) {
+#pragma clang fp contract(off)
+  using T = Tr<DT>;
+  constexpr int X = T::X;
+  const u32x4 w = *reinterpret_cast<const u32x4*>(row + c * X);
+  const int e0 = c * X;
+  if (e0 >= 2 * half) return w;
+  const bool lo = e0 < half;
+  const u32x4 wp = *reinterpret_cast<const u32x4*>(row + (lo ? e0 + half : e0 - half));
+  const int j0 = lo ? e0 : e0 - half;
+  float x[X], xp[X], y[X];
+  T::unpack(w, x);
+  T::unpack(wp, xp);
+#pragma unroll
+  for (int e = 0; e < X; ++e) {
+    const float a = x[e] * cs[2 * (j0 + e)];
+    const float b = xp[e] * cs[2 * (j0 + e) + 1];
+    y[e] = lo ? a - b : a + b;
+  }
+  return T::pack(y);
+}
+
+// Append with the rotary embedding: one wave per new token at position pos.
+// The wave rotates the token's query row (all Hq heads, in place), writes
+// its rotated key row into the cache and copies its value row, as the plain
+// append does.  A head's chunks all fall in one pass of the 64 lanes (D / X
+// divides 64), so a pass loads every partner chunk before it stores any.
+template <int DT, int D>
+__global__ __launch_bounds__(256) void rope_append_kernel(AppendArgs a, AppendPlan p, RopeArgs r) {
+  using T = Tr<DT>;
+  using E = typename T::Elem;
+  constexpr int X = T::X;
+  constexpr int NC = D / X;
+  static_assert(64 % NC == 0, "a head row's chunks fit one pass of the wave");
+  const int lane = threadIdx.x & 63;
+  const int tok = blockIdx.x * kWavesPerGroup + wave_uniform(threadIdx.x >> 6);
+  if (tok >= p.tok_start[p.n_seqs]) return;
+  const int j = p.unit ? tok : upper_index(p.tok_start, p.n_seqs, tok);
+  const int k = tok - p.tok_start[j];
+  const int s = p.seq[j];
+  const int t = p.row0[j] + k;
+  const int pos = p.pos0[j] + k;
+  const float* cs = r.cos_sin + (size_t)pos * r.half * 2;
+
+  E* q = reinterpret_cast<E*>(r.q) + (size_t)t * r.hq * D;
+  for (int c0 = 0; c0 < r.hq * NC; c0 += 64) {
+    const int ci = c0 + lane;
+    if (ci >= r.hq * NC) break;
+    const u32x4 y = rope_chunk<DT>(q + (ci / NC) * D, ci % NC, r.half, cs);
+    *reinterpret_cast<u32x4*>(q + (ci / NC) * D + (ci % NC) * X) = y;
+  }
+
+  const int blk = a.block_tables[(size_t)s * a.mb + pos / kBlock];
+  if (blk < 0 || blk >= a.nb) return;
+  const int slot = pos % kBlock;
+  const E* kn = reinterpret_cast<const E*>(a.k_new) + (size_t)t * a.hkv * D;
+  const E* vn = reinterpret_cast<const E*>(a.v_new) + (size_t)t * a.hkv * D;
+  for (int ci = lane; ci < a.hkv * NC; ci += 64) {
+    const int h = ci / NC, c = ci - h * NC;
+    const size_t head = (size_t)blk * a.hkv + h;
+    *reinterpret_cast<u32x4*>(reinterpret_cast<E*>(a.k_cache) + ((head * NC + c) * kBlock + slot) * X) =
+        rope_chunk<DT>(kn + h * D, c, r.half, cs);
+    E vv[X];
+#pragma unroll
+    for (int e = 0; e < X; ++e) vv[e] = vn[h * D + c * X + e];
+    E* vc = reinterpret_cast<E*>(a.v_cache) + (head * D + c * X) * kBlock + slot;
+#pragma unroll
+    for (int e = 0; e < X; ++e) vc[e * kBlock] = vv[e];
+  }
+}
+
 template <template <int, int> class F, typename... Args>
 hipError_t dispatch(int dtype, int head_dim, Args&&... args) {
   if (dtype == 0 && head_dim == 128) return F<0, 128>::run(args...);
@@ -943,6 +1043,17 @@ struct AppendL {
     if (tokens == 0) return hipSuccess;
     hipLaunchKernelGGL((append_kernel<DT, D>), dim3((tokens + kWavesPerGroup - 1) / kWavesPerGroup),
                        dim3(64 * kWavesPerGroup), 0, stream, a, p);
+    return hipGetLastError();
+  }
+};
+
+template <int DT, int D>
+struct RopeAppendL {
+  static hipError_t run(const AppendArgs& a, const AppendPlan& p, const RopeArgs& r, hipStream_t stream) {
+    const int tokens = p.tok_start[p.n_seqs];
+    if (tokens == 0) return hipSuccess;
+    hipLaunchKernelGGL((rope_append_kernel<DT, D>), dim3((tokens + kWavesPerGroup - 1) / kWavesPerGroup),
+                       dim3(64 * kWavesPerGroup), 0, stream, a, p, r);
     return hipGetLastError();
   }
 };
@@ -1014,6 +1125,11 @@ struct PrefillL {
 
 hipError_t launch_append(const AppendArgs& a, const AppendPlan& p, int dtype, int head_dim, hipStream_t stream) {
   return dispatch<AppendL>(dtype, head_dim, a, p, stream);
+}
+
+hipError_t launch_rope_append(const AppendArgs& a, const AppendPlan& p, const RopeArgs& r, int dtype, int head_dim,
+                              hipStream_t stream) {
+  return dispatch<RopeAppendL>(dtype, head_dim, a, p, r, stream);
 }
 
 int decode_wave_slots(int dtype, int head_dim) {

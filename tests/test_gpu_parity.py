@@ -176,6 +176,44 @@ def test_few_key_rows_at_rounding_floor(torch_gpu, seed):
     assert excess.max() <= 5e-4, f"few-key rows: {excess.max():.3g} above the bf16 rounding of the exact result"
 
 
+def rope_table(max_pos, rope_dim, base=10000.0):
+    j = np.arange(rope_dim // 2)
+    ang = np.arange(max_pos)[:, None] * base ** (-2.0 * j / rope_dim)[None, :]
+    return np.stack([np.cos(ang), np.sin(ang)], axis=-1).astype(np.float32)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("heads,rope_dim", [((32, 8, 128), 128), ((8, 2, 64), 32), ((16, 4, 128), 64)],
+                         ids=["d128_full", "d64_r32", "d128_r64"])
+def test_rope_append_then_attention(torch_gpu, dtype, heads, rope_dim):
+    """mpa_kv_append_rope: the rotated queries (in place) and the cache bit for
+    bit against the oracle's rotation, then attention on the rotated rows."""
+    torch = torch_gpu
+    rng = np.random.default_rng(80 + rope_dim)
+    b = make_batch(mixed_specs(rng), HeadSpec(*heads, 16), dtype, rng)
+    say(f"[gpu] rope append: S={b.num_seqs} T={b.total_q} heads={heads} R={rope_dim} dtype={dtype}")
+    table = rope_table(int(b.seq_lens.max()) + 7, rope_dim)
+    d = to_device(b)
+    mpa.kv_append_rope(d.q, d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
+                       d.seq_lens_host, d.qsl_host, torch.from_numpy(table).cuda(),
+                       block_tables_host=d.block_tables_host)
+    torch.cuda.synchronize()
+    pos = ref.new_token_positions(b.seq_lens, b.query_start_loc)
+    q_rot = ref.rope_reference(b.q, pos, table, rope_dim, dtype)
+    k_rot = ref.rope_reference(b.k_new, pos, table, rope_dim, dtype)
+    assert tensor_to_raw(d.q, dtype).tobytes() == np.ascontiguousarray(q_rot).tobytes(), "rotated q not bit-exact"
+    kc, vc = ref.append_reference(b.k_cache, b.v_cache, k_rot, b.v_new, b.block_tables, b.seq_lens,
+                                  b.query_start_loc, b.heads.block_size, dtype)
+    assert tensor_to_raw(d.k_cache, dtype).tobytes() == kc.tobytes(), "rotated K append not bit-exact"
+    assert tensor_to_raw(d.v_cache, dtype).tobytes() == vc.tobytes(), "V append not bit-exact"
+    out, lse = run_step(d, append=False)
+    o_ref, l_ref = ref.attention_reference(q_rot, b.k_cache, b.v_cache, k_rot, b.v_new, b.block_tables, b.seq_lens,
+                                           b.query_start_loc, b.scale, heads[1], 16, dtype)
+    rows = np.repeat(b.q_lens > 0, b.q_lens)
+    assert_close(as_f64(out)[rows], o_ref[rows], dtype, "rope attention")
+    assert np.abs(lse.cpu().numpy().astype(np.float64)[rows] - l_ref[rows]).max() <= LSE_TOL[dtype]
+
+
 @pytest.mark.parametrize("heads", SPLIT_MIXES, ids=lambda h: f"hq{h[0]}_hkv{h[1]}_d{h[2]}")
 def test_prefill_kv_splits(torch_gpu, heads):
     rng = np.random.default_rng(40 + heads[1])

@@ -197,3 +197,29 @@ def test_prefill_kv_splits_planned_for_short_chunks():
                  dtype=mpa.MPA_F32)
     assert mpa.plan_info(sh32, seq_lens, qsl).prefill_max_splits == 1
     assert mpa.workspace_size(sh32, seq_lens, qsl) == 0
+
+
+def test_rope_append_rejects_bad_arguments_before_any_launch():
+    """Host validation of mpa_kv_append_rope runs before anything touches a
+    device, so it can be exercised here with null device pointers."""
+    import ctypes
+
+    L = mpa.lib()
+    sl = np.array([100, 40], np.int32)
+    qsl = np.array([0, 1, 11], np.int32)
+    sh = mpa.make_shape(num_seqs=2, num_q_heads=8, num_kv_heads=2, head_dim=128, num_blocks=16,
+                        max_blocks_per_seq=8, total_q_tokens=11, scale=0.1, dtype=mpa.MPA_BF16)
+    fake = ctypes.c_void_p(16)  # never dereferenced: every case fails validation first
+
+    def call(rope_dim, max_pos, q=fake, table=fake):
+        return L.mpa_kv_append_rope(ctypes.byref(sh), q, fake, fake, fake, fake, fake, fake, fake,
+                                    sl.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                    qsl.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), None, table,
+                                    rope_dim, max_pos, None)
+
+    assert call(0, 128) == mpa.MPA_ERR_INVALID
+    assert call(24, 128) == mpa.MPA_ERR_INVALID       # not a multiple of 16
+    assert call(256, 128) == mpa.MPA_ERR_INVALID      # wider than head_dim
+    assert call(128, 99) == mpa.MPA_ERR_INVALID       # position 99 past a 99-row table
+    assert call(128, 128, q=None) == mpa.MPA_ERR_INVALID
+    assert call(128, 128, table=None) == mpa.MPA_ERR_INVALID
