@@ -30,8 +30,14 @@ the append (the rotary embedding, ``rope_reference``); the paper describes
 neither its models' position encoding nor such a kernel, so that function is
 the standard rotate-half definition with the rounding spelled out.
 
+The KV cache may also hold fp8 codes (OCP E4M3 with one scale per tensor,
+dtype "fp8"; queries, new rows and outputs stay bf16).  The paper is silent
+on cache precision; the reading is that a value x is stored as the E4M3
+code nearest to x / scale (ties to even, saturating at 448; ``fp8_codes``)
+and read back as code value * scale.
+
 Cache layout read here (the library header's definition), with
-``X = 16 / element_bytes``: K element (block b, head h, slot t, dim i) is at
+``X = 8`` elements (bf16, fp8) or 4 (f32): K element (block b, head h, slot t, dim i) is at
 ``[b][h][i // X][t][i % X]``; V element (b, h, t, i) is at ``[b][h][i][t]``.
 bf16 values arrive as their 16-bit patterns.
 """
@@ -40,11 +46,54 @@ from __future__ import annotations
 
 import numpy as np
 
-ELEM_BYTES = {"bf16": 2, "f32": 4}
+ELEM_BYTES = {"bf16": 2, "f32": 4, "fp8": 1}
+CHUNK = {"bf16": 8, "f32": 4, "fp8": 8}  # X: elements per K chunk of the cache layout
+
+
+def e4m3_values() -> np.ndarray:
+    """The 256 codes of OCP FP8 E4M3 (e4m3fn) as float64: sign in bit 7, a
+    4-bit exponent with bias 7 and a 3-bit mantissa; exponent 0 holds the
+    subnormals m * 2^-9; S.1111.111 is NaN and there is no infinity, so the
+    largest finite magnitude is 1.75 * 2^8 = 448."""
+    codes = np.arange(256)
+    e = (codes >> 3) & 0xF
+    m = codes & 7
+    v = np.where(e == 0, m * 2.0 ** -9, (1 + m / 8.0) * 2.0 ** (e - 7.0))
+    v = np.where(codes & 0x80, -v, v)
+    v[(codes & 0x7F) == 0x7F] = np.nan
+    return v
+
+
+def quantize_e4m3(y32: np.ndarray) -> np.ndarray:
+    """float32 -> E4M3 codes: the nearest finite value, a tie going to the
+    code with the even mantissa, magnitudes past 448 to 448 (saturating), NaN
+    to the NaN pattern; the sign is kept (so -0 -> 0x80)."""
+    y32 = np.asarray(y32, dtype=np.float32)
+    vals = e4m3_values()[:0x7F]  # +0 .. 448, increasing
+    a = np.abs(y32.astype(np.float64))
+    hi = np.clip(np.searchsorted(vals, a), 0, 0x7E)
+    lo = np.clip(hi - 1, 0, 0x7E)
+    dlo, dhi = a - vals[lo], vals[hi] - a
+    pick = np.where(dlo < dhi, lo, np.where(dhi < dlo, hi, np.where(lo % 2 == 0, lo, hi)))
+    pick = np.where(a >= 448.0, 0x7E, pick)
+    code = pick | np.where(np.signbit(y32), 0x80, 0)
+    code = np.where(np.isnan(y32), 0x7F | np.where(np.signbit(y32), 0x80, 0), code)
+    return code.astype(np.uint8)
+
+
+def fp8_codes(x_raw_bf16: np.ndarray, scale: float) -> np.ndarray:
+    """The cache codes of bf16 values under a per-tensor scale: x * (1/scale),
+    the reciprocal and the product each rounded to float32, then
+    quantize_e4m3."""
+    inv = np.float32(1.0) / np.float32(scale)
+    return quantize_e4m3(decode_raw(x_raw_bf16, "bf16").astype(np.float32) * inv)
 
 
 def decode_raw(raw: np.ndarray, dtype: str) -> np.ndarray:
-    """Raw storage -> float64.  A bf16 pattern is the top half of a float32."""
+    """Raw storage -> float64.  A bf16 pattern is the top half of a float32;
+    an fp8 code is an E4M3 value (before its tensor's scale)."""
+    if dtype == "fp8":
+        return e4m3_values()[np.asarray(raw, dtype=np.uint8)]
     if dtype == "bf16":
         u = np.ascontiguousarray(raw, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
         return u.view(np.float32).astype(np.float64)
@@ -54,7 +103,7 @@ def decode_raw(raw: np.ndarray, dtype: str) -> np.ndarray:
 
 
 def _x(dtype: str) -> int:
-    return 16 // ELEM_BYTES[dtype]
+    return CHUNK[dtype]
 
 
 def gather_kv(k_cache, v_cache, block_row, n_tokens, num_kv_heads, head_dim, block_size, dtype):
@@ -149,13 +198,20 @@ def attention_reference(
     block_size,
     dtype,
     seqs=None,
+    k_scale=1.0,
+    v_scale=1.0,
 ):
     """Outputs of one mixed step.
 
     Raw inputs in the library's layouts; the caches are the pool *before* the
     step's append.  Returns (out [T, Hq, d], lse [T, Hq]) float64; rows of
-    sequences not in ``seqs`` (default: all) are NaN."""
-    qf = decode_raw(q, dtype)
+    sequences not in ``seqs`` (default: all) are NaN.
+
+    dtype "fp8": q, k_new and v_new are bf16 and the caches hold E4M3 codes
+    with per-tensor scales; attention sees code value * scale, for the new
+    tokens too (their codes as the append writes them, fp8_codes)."""
+    qd = "bf16" if dtype == "fp8" else dtype
+    qf = decode_raw(q, qd)
     t, hq, d = qf.shape
     out = np.full((t, hq, d), np.nan)
     lse = np.full((t, hq), np.nan)
@@ -170,18 +226,28 @@ def attention_reference(
         big_l = int(seq_lens[s])
         prefix = big_l - c
         kp, vp = gather_kv(k_cache, v_cache, block_tables[s], prefix, num_kv_heads, d, block_size, dtype)
-        k = np.concatenate([kp, decode_raw(k_new[t0:t1], dtype)], axis=0)
-        v = np.concatenate([vp, decode_raw(v_new[t0:t1], dtype)], axis=0)
+        if dtype == "fp8":
+            kn = decode_raw(fp8_codes(k_new[t0:t1], k_scale), "fp8")
+            vn = decode_raw(fp8_codes(v_new[t0:t1], v_scale), "fp8")
+            k = np.concatenate([kp, kn], axis=0) * k_scale
+            v = np.concatenate([vp, vn], axis=0) * v_scale
+        else:
+            k = np.concatenate([kp, decode_raw(k_new[t0:t1], dtype)], axis=0)
+            v = np.concatenate([vp, decode_raw(v_new[t0:t1], dtype)], axis=0)
         out[t0:t1], lse[t0:t1] = sequence_attention(qf[t0:t1], k, v, prefix, scale, num_kv_heads)
     return out, lse
 
 
-def append_reference(k_cache, v_cache, k_new, v_new, block_tables, seq_lens, query_start_loc, block_size, dtype):
+def append_reference(k_cache, v_cache, k_new, v_new, block_tables, seq_lens, query_start_loc, block_size, dtype,
+                     k_scale=1.0, v_scale=1.0):
     """The pool after the step's append, as raw copies of the inputs.
 
     Token i of sequence s goes to logical position P_s + i, i.e. slot
     ``(P_s + i) % bs`` of block ``block_tables[s][(P_s + i) // bs]``; its bits
-    are copied unchanged.  Nothing else in the pool changes."""
+    are copied unchanged (dtype "fp8": its fp8_codes are stored).  Nothing
+    else in the pool changes."""
+    if dtype == "fp8":
+        k_new, v_new = fp8_codes(k_new, k_scale), fp8_codes(v_new, v_scale)
     x = _x(dtype)
     kc = k_cache.copy()
     vc = v_cache.copy()

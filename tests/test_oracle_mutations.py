@@ -77,9 +77,29 @@ def _rope_sign(x_raw, positions, cos_sin, rope_dim, dtype):
 _good_rope = ref.rope_reference
 
 
+def _e4m3_fnuz_values():
+    # wrong: the "fnuz" variant's exponent bias 8 (and no negative zero)
+    v = _good_e4m3() / 2.0
+    v[0x80] = np.nan
+    return v
+
+
+def _quantize_truncating(y32):
+    # wrong: rounds magnitudes toward zero instead of to nearest even
+    vals = _good_e4m3()[:0x7F]
+    a = np.abs(np.asarray(y32, np.float64))
+    pick = np.clip(np.searchsorted(vals, a, side="right") - 1, 0, 0x7E)
+    return (pick | np.where(np.signbit(y32), 0x80, 0)).astype(np.uint8)
+
+
+_good_e4m3 = ref.e4m3_values
+
+
 MUTANTS = {
     "rope_interleaved_pairs": ("rope_reference", _rope_interleaved),
     "rope_reversed": ("rope_reference", _rope_sign),
+    "e4m3_fnuz_bias": ("e4m3_values", _e4m3_fnuz_values),
+    "e4m3_truncating": ("quantize_e4m3", _quantize_truncating),
     "top_left_causal": ("sequence_attention", _seq_attn_factory(
         visible_fn=lambda keys, rows, prefix: keys[None] <= rows[:, None])),
     "exclusive_diagonal": ("sequence_attention", _seq_attn_factory(
@@ -99,6 +119,8 @@ PIN_TESTS = [
     lambda: pins.test_zero_query_gives_running_mean(),
     lambda: pins.test_rope_hand_worked(),
     lambda: pins.test_rope_zero_and_quarter_turn("f32"),
+    lambda: pins.test_e4m3_table_fixed_points(),
+    lambda: pins.test_e4m3_quantize_round_trip_ties_and_saturation(),
 ]
 
 

@@ -482,3 +482,79 @@ def test_rope_preserves_pair_norms_and_relative_position():
 def test_rope_positions_of_new_tokens():
     pos = ref.new_token_positions([5, 9, 3], [0, 1, 4, 4])
     assert pos.tolist() == [4, 6, 7, 8]
+
+
+# ----------------------------------------------------------------------------
+# fp8 (OCP E4M3) cache codes
+
+
+def test_e4m3_table_fixed_points():
+    v = ref.e4m3_values()
+    # from the format's definition: bias 7, 3 mantissa bits, S.1111.111 NaN
+    assert v[0x38] == 1.0 and v[0xB8] == -1.0 and v[0x7E] == 448.0 and v[0xFE] == -448.0
+    assert v[0x01] == 2.0 ** -9 and v[0x07] == 7 * 2.0 ** -9 and v[0x08] == 2.0 ** -6
+    assert v[0x3C] == 1.5 and v[0x40] == 2.0 and v[0x30] == 0.5
+    assert v[0x00] == 0.0 and v[0x80] == 0.0 and math.copysign(1, v[0x80]) < 0
+    assert np.isnan(v[0x7F]) and np.isnan(v[0xFF]) and np.isfinite(np.delete(v, [0x7F, 0xFF])).all()
+
+
+def test_e4m3_quantize_round_trip_ties_and_saturation():
+    v = ref.e4m3_values()
+    finite = np.array([c for c in range(256) if not np.isnan(v[c])], np.uint8)
+    assert np.array_equal(ref.quantize_e4m3(v[finite].astype(np.float32)), finite)  # every code reproduces
+    x = np.array([1 + 1 / 16, 1 + 3 / 16, 7.5 * 2 ** -9, 0.5 * 2 ** -9, 1.5 * 2 ** -9, 464, 463.99, 1e6, -1e6,
+                  -2 ** -12], np.float32)
+    # ties to the even mantissa (also at the subnormal/normal seam and at 0),
+    # saturation at +-448, and the sign kept on an underflow to zero
+    assert ref.quantize_e4m3(x).tolist() == [0x38, 0x3A, 0x08, 0x00, 0x02, 0x7E, 0x7E, 0x7E, 0xFE, 0x80]
+    y = np.sort(np.random.default_rng(50).standard_normal(20000).astype(np.float32) * 100)
+    c = ref.quantize_e4m3(y)
+    assert np.all(np.diff(v[c]) >= 0)  # monotone
+
+
+def test_e4m3_matches_torch_in_range():
+    torch = pytest.importorskip("torch")
+    if not hasattr(torch, "float8_e4m3fn"):
+        pytest.skip("torch without float8_e4m3fn")
+    x = np.random.default_rng(51).standard_normal(200000).astype(np.float32) * np.float32(60.0)
+    x = x[np.abs(x) < 440]
+    t = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    assert np.array_equal(ref.quantize_e4m3(x), t)
+
+
+def test_fp8_attention_is_attention_on_the_scaled_codes():
+    """The fp8 path is ordinary attention on code value * scale, with the new
+    tokens entering as the codes the append stores."""
+    rng = np.random.default_rng(52)
+    hkv, d, bs = 2, 64, 16
+    specs = [(70, 1), (40, 5)]
+    nb = sum(-(-c // bs) for c, _ in specs)
+    qsl = np.concatenate([[0], np.cumsum([ql for _, ql in specs])]).astype(np.int32)
+    t = int(qsl[-1])
+    q = bf16_bits_from_f32(rng.standard_normal((t, 4, d), dtype=np.float32))
+    kn = bf16_bits_from_f32(rng.standard_normal((t, hkv, d), dtype=np.float32))
+    vn = bf16_bits_from_f32(rng.standard_normal((t, hkv, d), dtype=np.float32))
+    kc = rng.integers(0, 0x7E, size=(nb, hkv, d // 8, bs, 8)).astype(np.uint8)
+    vc = rng.integers(0, 0x7E, size=(nb, hkv, d, bs)).astype(np.uint8)
+    kc |= (rng.random(kc.shape) < 0.5).astype(np.uint8) << 7
+    bt = np.arange(nb, dtype=np.int32).reshape(1, -1).repeat(2, 0)
+    bt[1] = np.roll(bt[1], 3)
+    sl = np.array([c for c, _ in specs], np.int32)
+    ks, vs = 0.0173, 0.0211
+    o8, l8 = ref.attention_reference(q, kc, vc, kn, vn, bt, sl, qsl, 0.125, hkv, bs, "fp8", k_scale=ks, v_scale=vs)
+    # the same through the f32 path, on the dequantized pool and new rows
+    kc32 = (ref.e4m3_values()[kc] * ks).astype(np.float32)
+    vc32 = (ref.e4m3_values()[vc] * vs).astype(np.float32)
+    kc32 = kc32.reshape(nb, hkv, d // 8, bs, 2, 4).transpose(0, 1, 2, 4, 3, 5).reshape(nb, hkv, d // 4, bs, 4)
+    kn32 = (ref.e4m3_values()[ref.fp8_codes(kn, ks)] * ks).astype(np.float32)
+    vn32 = (ref.e4m3_values()[ref.fp8_codes(vn, vs)] * vs).astype(np.float32)
+    q32 = ref.decode_raw(q, "bf16").astype(np.float32)
+    o32, l32 = ref.attention_reference(q32, kc32, vc32, kn32, vn32, bt, sl, qsl, 0.125, hkv, bs, "f32")
+    assert np.allclose(o8, o32, atol=1e-6) and np.allclose(l8, l32, atol=1e-6)
+    # and the append stores exactly those codes
+    kc2, vc2 = ref.append_reference(kc, vc, kn, vn, bt, sl, qsl, bs, "fp8", k_scale=ks, v_scale=vs)
+    pos = ref.new_token_positions(sl, qsl)
+    seq = np.repeat(np.arange(2), np.diff(qsl))
+    blk = bt[seq, pos // bs]
+    assert np.array_equal(kc2.reshape(nb, hkv, d // 8, bs, 8)[blk, :, :, pos % bs, :].reshape(t, hkv, d),
+                          ref.fp8_codes(kn, ks))
