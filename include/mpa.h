@@ -37,7 +37,7 @@
  *   v_new    [T][Hkv][d]
  *   out      [T][Hq][d]
  *   lse      [T][Hq] float32, natural log of each row's softmax denominator
- *   k_cache  [num_blocks][Hkv][d/X][16][X]   X = 16 / element bytes
+ *   k_cache  [num_blocks][Hkv][d/X][16][X]   X = 8 (bf16, fp8) or 4 (f32)
  *   v_cache  [num_blocks][Hkv][d][16]
  * i.e. key element (block b, head h, slot t, dim i) is at
  * k_cache[b][h][i/X][t][i%X] and value element (b, h, t, i) at
@@ -46,8 +46,18 @@
  * rows; the slots a step appends to must be distinct.
  *
  * Supported: dtype bf16 or f32 (the caches, q, k_new, v_new and out all in
- * that type), head_dim 64 or 128, block_size 16, Hq a multiple of Hkv with
+ * that type), or fp8 (the caches hold OCP FP8 E4M3 codes, one byte per
+ * element, with one scale per cache; q, k_new, v_new and out are bf16);
+ * head_dim 64 or 128, block_size 16, Hq a multiple of Hkv with
  * Hq / Hkv <= 16.
+ *
+ * fp8 caches: the paper is silent on cache precision.  A key value x is
+ * stored as the E4M3 code nearest to x * (1 / k_scale) -- the reciprocal
+ * and the product each rounded to float32 -- with ties to the even
+ * mantissa and magnitudes past 448 saturated to 448 (NaN stays NaN); it is
+ * read back as code value * k_scale (values likewise with v_scale).  E4M3:
+ * sign bit, 4-bit exponent with bias 7, 3-bit mantissa, subnormals m*2^-9,
+ * S.1111.111 = NaN, no infinity.
  *
  * Conventions:
  *  - The caller owns every buffer.  The library allocates nothing and keeps
@@ -82,7 +92,7 @@ typedef enum {
   MPA_ERR_HIP = -4          /* a HIP launch reported an error */
 } mpa_status;
 
-typedef enum { MPA_BF16 = 0, MPA_F32 = 1 } mpa_dtype;
+typedef enum { MPA_BF16 = 0, MPA_F32 = 1, MPA_FP8 = 2 } mpa_dtype;
 
 typedef struct {
   int32_t num_seqs;           /* S */
@@ -95,6 +105,8 @@ typedef struct {
   int32_t total_q_tokens;     /* T = query_start_loc[S] */
   float scale;                /* softmax scale, finite and > 0, e.g. 1/sqrt(d) */
   int32_t dtype;              /* mpa_dtype */
+  float k_scale;              /* fp8: key cache scale, finite and > 0 (else unused) */
+  float v_scale;              /* fp8: value cache scale, finite and > 0 (else unused) */
 } mpa_shape;
 
 /*

@@ -30,6 +30,7 @@ MPA_ERR_WORKSPACE = -3
 MPA_ERR_HIP = -4
 MPA_BF16 = 0
 MPA_F32 = 1
+MPA_FP8 = 2  # fp8 (OCP E4M3) caches with bf16 queries, new rows and outputs
 BLOCK_SIZE = 16
 
 EXPORTS = (
@@ -68,6 +69,8 @@ class MpaShape(ctypes.Structure):
         ("total_q_tokens", ctypes.c_int32),
         ("scale", ctypes.c_float),
         ("dtype", ctypes.c_int32),
+        ("k_scale", ctypes.c_float),
+        ("v_scale", ctypes.c_float),
     ]
 
 
@@ -164,6 +167,8 @@ def _i32p(a: Optional[np.ndarray]):
 def _dtype_code(t) -> int:
     import torch
 
+    if t.dtype == torch.uint8 or t.dtype == getattr(torch, "float8_e4m3fn", None):
+        return MPA_FP8
     if t.dtype == torch.bfloat16:
         return MPA_BF16
     if t.dtype == torch.float32:
@@ -190,19 +195,22 @@ def _stream(stream) -> Optional[int]:
 
 
 def make_shape(num_seqs, num_q_heads, num_kv_heads, head_dim, num_blocks, max_blocks_per_seq, total_q_tokens,
-               scale, dtype: int, block_size: int = BLOCK_SIZE) -> MpaShape:
+               scale, dtype: int, block_size: int = BLOCK_SIZE, k_scale: float = 1.0,
+               v_scale: float = 1.0) -> MpaShape:
     return MpaShape(int(num_seqs), int(num_q_heads), int(num_kv_heads), int(head_dim), int(block_size),
-                    int(num_blocks), int(max_blocks_per_seq), int(total_q_tokens), float(scale), int(dtype))
+                    int(num_blocks), int(max_blocks_per_seq), int(total_q_tokens), float(scale), int(dtype),
+                    float(k_scale), float(v_scale))
 
 
-def shape_of(q, k_cache, block_tables, seq_lens_host, scale=None) -> MpaShape:
+def shape_of(q, k_cache, block_tables, seq_lens_host, scale=None, k_scale=1.0, v_scale=1.0) -> MpaShape:
     """mpa_shape from the tensors: q [T, Hq, d], k_cache [NB, Hkv, d/X, 16, X]
-    (or any view with NB and Hkv leading), block_tables [S, MB]."""
+    (or any view with NB and Hkv leading), block_tables [S, MB].  The dtype
+    comes from the cache (uint8 = fp8 codes), the queries being bf16 then."""
     t, hq, d = q.shape
     if scale is None:
         scale = 1.0 / float(d) ** 0.5
     return make_shape(len(seq_lens_host), hq, k_cache.shape[1], d, k_cache.shape[0], block_tables.shape[1], t,
-                      scale, _dtype_code(q))
+                      scale, _dtype_code(k_cache), k_scale=k_scale, v_scale=v_scale)
 
 
 def plan_info(shape: MpaShape, seq_lens_host, qsl_host) -> MpaPlanInfo:
@@ -249,12 +257,14 @@ def alloc_workspace(q, k_cache, block_tables, seq_lens_host, qsl_host, scale=Non
 
 
 def kv_append(k_new, v_new, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host,
-              block_tables_host=None, stream=None) -> None:
-    """mpa_kv_append on torch device tensors (host metadata as arrays)."""
+              block_tables_host=None, stream=None, k_scale=1.0, v_scale=1.0) -> None:
+    """mpa_kv_append on torch device tensors (host metadata as arrays); with
+    uint8 (fp8) caches the bf16 rows are stored as codes under the scales."""
     t, hkv, d = k_new.shape
     sl, qs = _host_i32(seq_lens_host), _host_i32(qsl_host)
     bth = None if block_tables_host is None else _host_i32(block_tables_host)
-    shape = make_shape(len(sl), hkv, hkv, d, k_cache.shape[0], block_tables.shape[1], t, 1.0, _dtype_code(k_new))
+    shape = make_shape(len(sl), hkv, hkv, d, k_cache.shape[0], block_tables.shape[1], t, 1.0, _dtype_code(k_cache),
+                       k_scale=k_scale, v_scale=v_scale)
     rc = lib().mpa_kv_append(
         ctypes.byref(shape), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(block_tables),
         _ptr(seq_lens), _ptr(query_start_loc), _i32p(sl), _i32p(qs), _i32p(bth), _stream(stream))
@@ -273,7 +283,7 @@ def kv_append_rope(q, k_new, v_new, k_cache, v_cache, block_tables, seq_lens, qu
         rope_dim = 2 * int(cos_sin.shape[1])
     sl, qs = _host_i32(seq_lens_host), _host_i32(qsl_host)
     bth = None if block_tables_host is None else _host_i32(block_tables_host)
-    shape = make_shape(len(sl), hq, hkv, d, k_cache.shape[0], block_tables.shape[1], t, 1.0, _dtype_code(k_new))
+    shape = make_shape(len(sl), hq, hkv, d, k_cache.shape[0], block_tables.shape[1], t, 1.0, _dtype_code(k_cache))
     rc = lib().mpa_kv_append_rope(
         ctypes.byref(shape), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(block_tables),
         _ptr(seq_lens), _ptr(query_start_loc), _i32p(sl), _i32p(qs), _i32p(bth), _ptr(cos_sin), int(rope_dim),
@@ -283,10 +293,10 @@ def kv_append_rope(q, k_new, v_new, k_cache, v_cache, block_tables, seq_lens, qu
 
 
 def _attention(which, q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host, out,
-               lse, workspace, scale, block_tables_host, stream) -> None:
+               lse, workspace, scale, block_tables_host, stream, k_scale=1.0, v_scale=1.0) -> None:
     sl, qs = _host_i32(seq_lens_host), _host_i32(qsl_host)
     bth = None if block_tables_host is None else _host_i32(block_tables_host)
-    shape = shape_of(q, k_cache, block_tables, sl, scale)
+    shape = shape_of(q, k_cache, block_tables, sl, scale, k_scale, v_scale)
     args = [ctypes.byref(shape), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_tables), _ptr(seq_lens),
             _ptr(query_start_loc), _i32p(sl), _i32p(qs), _i32p(bth), _ptr(out), _ptr(lse)]
     args += [None, 0] if workspace is None else [_ptr(workspace), workspace.numel() * workspace.element_size()]
@@ -297,21 +307,25 @@ def _attention(which, q, k_cache, v_cache, block_tables, seq_lens, query_start_l
 
 
 def mixed_paged_attention(q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host,
-                          out, lse=None, workspace=None, scale=None, block_tables_host=None, stream=None) -> None:
-    """mpa_mixed_paged_attention on torch device tensors."""
+                          out, lse=None, workspace=None, scale=None, block_tables_host=None, stream=None,
+                          k_scale=1.0, v_scale=1.0) -> None:
+    """mpa_mixed_paged_attention on torch device tensors (k_scale, v_scale:
+    the scales of uint8 = fp8 caches)."""
     _attention("mpa_mixed_paged_attention", q, k_cache, v_cache, block_tables, seq_lens, query_start_loc,
-               seq_lens_host, qsl_host, out, lse, workspace, scale, block_tables_host, stream)
+               seq_lens_host, qsl_host, out, lse, workspace, scale, block_tables_host, stream, k_scale, v_scale)
 
 
 def decode_attention(q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host,
-                     out, lse=None, workspace=None, scale=None, block_tables_host=None, stream=None) -> None:
+                     out, lse=None, workspace=None, scale=None, block_tables_host=None, stream=None,
+                     k_scale=1.0, v_scale=1.0) -> None:
     """mpa_decode_attention: only the rows of sequences with q_len == 1."""
     _attention("mpa_decode_attention", q, k_cache, v_cache, block_tables, seq_lens, query_start_loc,
-               seq_lens_host, qsl_host, out, lse, workspace, scale, block_tables_host, stream)
+               seq_lens_host, qsl_host, out, lse, workspace, scale, block_tables_host, stream, k_scale, v_scale)
 
 
 def prefill_attention(q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host,
-                      out, lse=None, workspace=None, scale=None, block_tables_host=None, stream=None) -> None:
+                      out, lse=None, workspace=None, scale=None, block_tables_host=None, stream=None,
+                      k_scale=1.0, v_scale=1.0) -> None:
     """mpa_prefill_attention: only the rows of sequences with q_len > 1."""
     _attention("mpa_prefill_attention", q, k_cache, v_cache, block_tables, seq_lens, query_start_loc,
-               seq_lens_host, qsl_host, out, lse, workspace, scale, block_tables_host, stream)
+               seq_lens_host, qsl_host, out, lse, workspace, scale, block_tables_host, stream, k_scale, v_scale)

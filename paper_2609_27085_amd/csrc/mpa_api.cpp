@@ -30,7 +30,10 @@ int check_shape(const mpa_shape* sh) {
   if (sh->num_seqs < 0 || sh->num_q_heads <= 0 || sh->num_kv_heads <= 0 || sh->num_blocks < 0 ||
       sh->max_blocks_per_seq < 0 || sh->total_q_tokens < 0 || !isfinite(sh->scale) || !(sh->scale > 0.f))
     return MPA_ERR_INVALID;
-  if (sh->dtype != MPA_BF16 && sh->dtype != MPA_F32) return MPA_ERR_UNSUPPORTED;
+  if (sh->dtype != MPA_BF16 && sh->dtype != MPA_F32 && sh->dtype != MPA_FP8) return MPA_ERR_UNSUPPORTED;
+  if (sh->dtype == MPA_FP8 && !(isfinite(sh->k_scale) && sh->k_scale > 0.f && isfinite(sh->v_scale) &&
+                                sh->v_scale > 0.f))
+    return MPA_ERR_INVALID;
   if (sh->head_dim != 64 && sh->head_dim != 128) return MPA_ERR_UNSUPPORTED;
   if (sh->block_size != kBlock) return MPA_ERR_UNSUPPORTED;
   if (sh->num_q_heads % sh->num_kv_heads != 0) return MPA_ERR_UNSUPPORTED;
@@ -195,6 +198,8 @@ int run_append(const mpa_shape* shape, const void* k_new, const void* v_new, voi
   a.hkv = shape->num_kv_heads;
   a.mb = shape->max_blocks_per_seq;
   a.nb = shape->num_blocks;
+  a.inv_k_scale = shape->dtype == MPA_FP8 ? 1.f / shape->k_scale : 1.f;
+  a.inv_v_scale = shape->dtype == MPA_FP8 ? 1.f / shape->v_scale : 1.f;
   (void)seq_lens;
   (void)query_start_loc;
   std::vector<int> seqs(b.decode);
@@ -394,6 +399,7 @@ int mpa_kv_append_rope(const mpa_shape* shape, void* q, const void* k_new, const
   if (!shape) return MPA_ERR_INVALID;
   if (rope_dim <= 0 || rope_dim % 16 != 0 || rope_dim > shape->head_dim || rope_max_pos <= 0)
     return MPA_ERR_INVALID;
+  if (shape->dtype == MPA_FP8) return MPA_ERR_UNSUPPORTED;  // the rotation is built for bf16 and f32 caches
   if (shape->total_q_tokens > 0 && (!q || !rope_cos_sin)) return MPA_ERR_INVALID;
   if (seq_lens_host && shape->num_seqs > 0)
     for (int s = 0; s < shape->num_seqs; ++s)
@@ -460,7 +466,11 @@ int run_attention(int phases, const mpa_shape* shape, const void* q, const void*
   a.hkv = shape->num_kv_heads;
   a.mb = shape->max_blocks_per_seq;
   a.nb = shape->num_blocks;
-  a.scale_log2 = shape->scale * 1.4426950408889634f;
+  // fp8 caches: the key scale folds into the softmax scale, the value scale
+  // into the output (and the split partials)
+  const bool fp8 = shape->dtype == MPA_FP8;
+  a.scale_log2 = shape->scale * 1.4426950408889634f * (fp8 ? shape->k_scale : 1.f);
+  a.v_scale = fp8 ? shape->v_scale : 1.f;
   hipStream_t st = (hipStream_t)stream;
   clear_stale_hip_error();
 

@@ -31,7 +31,8 @@ struct AttnArgs {
   float* ws_o;       // [items][Hq][d] split partial accumulators
   float* ws_ml;      // [items][Hq][2] split partial (max, sum); max in log2 units
   int32_t hq, hkv, mb, nb;
-  float scale_log2;  // softmax scale * log2(e)
+  float scale_log2;  // softmax scale * log2(e) (* the key scale for fp8 caches)
+  float v_scale;     // fp8 caches: the value scale (1 otherwise), applied to outputs and partials
 };
 
 // Decode work for up to kMaxPlanSeqs sequences: item k of this launch is
@@ -74,6 +75,7 @@ struct AppendArgs {
   void* v_cache;
   const int32_t* block_tables;
   int32_t hkv, mb, nb;
+  float inv_k_scale, inv_v_scale;  // fp8 caches: 1 / scale, rounded to f32 (1 otherwise)
 };
 
 // The rotary embedding applied by the rope append: query rows (in place,
@@ -97,7 +99,7 @@ struct AppendPlan {
   int32_t tok_start[kMaxPlanSeqs + 1];
 };
 
-// Launchers (mpa_kernels.hip).  dtype: 0 = bf16, 1 = f32.  Return the HIP
+// Launchers (mpa_kernels.hip).  dtype: 0 = bf16, 1 = f32, 2 = fp8 cache.  Return the HIP
 // error of the launch.
 hipError_t launch_append(const AppendArgs& a, const AppendPlan& p, int dtype, int head_dim, hipStream_t stream);
 hipError_t launch_rope_append(const AppendArgs& a, const AppendPlan& p, const RopeArgs& r, int dtype, int head_dim,

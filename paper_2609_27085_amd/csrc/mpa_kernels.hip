@@ -95,7 +95,8 @@ struct Tr;
 
 template <>
 struct Tr<0> {  // bf16
-  using Elem = uint16_t;
+  using Elem = uint16_t;   // cache element
+  using QElem = uint16_t;  // queries, new rows and outputs
   static constexpr int X = 8;
   using Chunk = bf16x8;
   using VFrag = s16x4;
@@ -103,6 +104,7 @@ struct Tr<0> {  // bf16
   static __device__ inline Chunk load_chunk(const Elem* p) {
     return __builtin_bit_cast(Chunk, *reinterpret_cast<const u32x4*>(p));
   }
+  static __device__ inline Chunk load_q(const QElem* p) { return load_chunk(p); }
   static __device__ inline Chunk zero_chunk() {
     u32x4 z = {0u, 0u, 0u, 0u};
     return __builtin_bit_cast(Chunk, z);
@@ -164,11 +166,13 @@ struct Tr<0> {  // bf16
 template <>
 struct Tr<1> {  // f32
   using Elem = float;
+  using QElem = float;
   static constexpr int X = 4;
   using Chunk = f32x4;
   using VFrag = f32x4;
   using PFrag = f32x4;
   static __device__ inline Chunk load_chunk(const Elem* p) { return *reinterpret_cast<const f32x4*>(p); }
+  static __device__ inline Chunk load_q(const QElem* p) { return load_chunk(p); }
   static __device__ inline Chunk zero_chunk() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
   static __device__ inline f32x4 qk(Chunk k, Chunk q, f32x4 c) {
 #pragma unroll
@@ -203,6 +207,60 @@ struct Tr<1> {  // f32
     return w;
   }
 };
+
+// fp8 caches (OCP E4M3 codes) beside bf16 queries, new rows and outputs.
+// Codes become bf16 on load (exact: every E4M3 value is a bf16 value) and
+// the arithmetic is the bf16 path's; the tensors' scales are applied outside
+// (key scale in the softmax scale, value scale on the outputs).
+template <>
+struct Tr<2> {
+  using Elem = uint8_t;
+  using QElem = uint16_t;
+  static constexpr int X = 8;  // codes per K chunk: 8 bytes
+  using Chunk = bf16x8;
+  using VFrag = s16x4;
+  using PFrag = s16x4;
+  static constexpr bool kRoundsP = true;
+  static __device__ inline unsigned cvt2(unsigned w, bool hi) {
+    return hi ? __builtin_bit_cast(unsigned, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w, 1.0f, true))
+              : __builtin_bit_cast(unsigned, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w, 1.0f, false));
+  }
+  static __device__ inline Chunk load_chunk(const Elem* p) {
+    const u32x2 w = *reinterpret_cast<const u32x2*>(p);
+    const u32x4 r = {cvt2(w[0], false), cvt2(w[0], true), cvt2(w[1], false), cvt2(w[1], true)};
+    return __builtin_bit_cast(Chunk, r);
+  }
+  static __device__ inline Chunk load_q(const QElem* p) { return Tr<0>::load_q(p); }
+  static __device__ inline Chunk zero_chunk() { return Tr<0>::zero_chunk(); }
+  static __device__ inline f32x4 qk(Chunk k, Chunk q, f32x4 c) { return Tr<0>::qk(k, q, c); }
+  static __device__ inline VFrag load_v(const Elem* p) {
+    const unsigned w = *reinterpret_cast<const unsigned*>(p);
+    const u32x2 r = {cvt2(w, false), cvt2(w, true)};
+    return __builtin_bit_cast(VFrag, r);
+  }
+  static __device__ inline VFrag keep_first(VFrag v, int nvalid) { return Tr<0>::keep_first(v, nvalid); }
+  static __device__ inline PFrag make_p(f32x4 p) { return Tr<0>::make_p(p); }
+  static __device__ inline PFrag make_p_lo(f32x4 p, PFrag hi) { return Tr<0>::make_p_lo(p, hi); }
+  static __device__ inline f32x4 pv(VFrag v, PFrag p, f32x4 c) { return Tr<0>::pv(v, p, c); }
+  static __device__ inline float psum(f32x4 p, PFrag pf, float acc) { return Tr<0>::psum(p, pf, acc); }
+  static __device__ inline void store4(QElem* dst, f32x4 v) { Tr<0>::store4(dst, v); }
+  static __device__ inline void store1(QElem* dst, float v) { Tr<0>::store1(dst, v); }
+};
+
+// float32 -> OCP E4M3 code: round to nearest, ties to the even mantissa;
+// magnitudes from 464 up (which would round past the largest finite value,
+// 448) saturate to 448; NaN -> the NaN code; the sign is kept.
+__device__ inline unsigned f32_to_e4m3(float x) {
+  const unsigned u = __float_as_uint(x);
+  const unsigned sign = (u >> 24) & 0x80u;
+  const float a = fabsf(x);
+  if (a != a) return sign | 0x7Fu;
+  if (a >= 464.f) return sign | 0x7Eu;
+  if (a < 0.015625f) return sign | (unsigned)rintf(a * 512.f);  // subnormals m * 2^-9 (8 = 2^-6)
+  unsigned ua = __float_as_uint(a);
+  ua += 0x7FFFFu + ((ua >> 20) & 1u);  // round the f32 mantissa to 3 bits, ties to even
+  return sign | ((((ua >> 23) - 120u) << 3) | ((ua >> 20) & 7u));
+}
 
 // Largest j in [0, n) with starts[j] <= x (starts non-decreasing, starts[0] <= x).
 __device__ inline int upper_index(const int32_t* starts, int n, int x) {
@@ -371,7 +429,7 @@ __device__ inline void attend_blocks(const AttnArgs& a, const typename Tr<DT>::C
 template <int DT, int D>
 __global__ __launch_bounds__(256) void decode_kernel(AttnArgs a, DecodePlan p) {
   using T = Tr<DT>;
-  using E = typename T::Elem;
+  using QE = typename T::QElem;
   constexpr int X = T::X;
   constexpr int R = D / (4 * X);
   constexpr int MT = D / 16;
@@ -394,10 +452,10 @@ __global__ __launch_bounds__(256) void decode_kernel(AttnArgs a, DecodePlan p) {
   const bool head_ok = n < G;
   const int h = g * G + (head_ok ? n : 0);
 
-  const E* q = reinterpret_cast<const E*>(a.q) + ((size_t)trow * a.hq + h) * D;
+  const QE* q = reinterpret_cast<const QE*>(a.q) + ((size_t)trow * a.hq + h) * D;
   typename T::Chunk qf[R];
 #pragma unroll
-  for (int r = 0; r < R; ++r) qf[r] = head_ok ? T::load_chunk(q + (4 * r + grp) * X) : T::zero_chunk();
+  for (int r = 0; r < R; ++r) qf[r] = head_ok ? T::load_q(q + (4 * r + grp) * X) : T::zero_chunk();
 
   RowState<DT, D> st;
 #pragma unroll
@@ -412,8 +470,8 @@ __global__ __launch_bounds__(256) void decode_kernel(AttnArgs a, DecodePlan p) {
   l += __shfl_xor(l, 32);
   if (!head_ok) return;
   if (nsplit == 1) {
-    const float inv = poison ? NAN : 1.f / l;
-    E* o = reinterpret_cast<E*>(a.out) + ((size_t)trow * a.hq + h) * D;
+    const float inv = poison ? NAN : a.v_scale / l;
+    QE* o = reinterpret_cast<QE*>(a.out) + ((size_t)trow * a.hq + h) * D;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) T::store4(o + 16 * mt + 4 * grp, st.acc[mt] * inv);
     if (a.lse && grp == 0) a.lse[(size_t)trow * a.hq + h] = poison ? NAN : (st.m + log2f(l)) * kLn2;
@@ -422,7 +480,8 @@ __global__ __launch_bounds__(256) void decode_kernel(AttnArgs a, DecodePlan p) {
     float* wo = a.ws_o + slot * D;
     const float bad = poison ? NAN : 1.f;
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) *reinterpret_cast<f32x4*>(wo + 16 * mt + 4 * grp) = st.acc[mt] * bad;
+    for (int mt = 0; mt < MT; ++mt)
+      *reinterpret_cast<f32x4*>(wo + 16 * mt + 4 * grp) = st.acc[mt] * (bad * a.v_scale);
     if (grp == 0) {
       a.ws_ml[slot * 2] = st.m;
       a.ws_ml[slot * 2 + 1] = l * bad;
@@ -445,7 +504,7 @@ __global__ __launch_bounds__(256) void decode_kernel(AttnArgs a, DecodePlan p) {
 // l + 64, ... of out; lane 0 writes lse.
 template <int DT, int D>
 __device__ inline void merge_splits(const float* ml, size_t ml_stride, const float* acc, size_t acc_stride, int n,
-                                    typename Tr<DT>::Elem* out, float* lse) {
+                                    typename Tr<DT>::QElem* out, float* lse) {
   using T = Tr<DT>;
   constexpr int PER = D / 64;
   constexpr int GRP = 16;
@@ -489,7 +548,7 @@ __device__ inline void merge_splits(const float* ml, size_t ml_stride, const flo
 // Decode merge: one 64-lane workgroup per (split decode sequence, q head).
 template <int DT, int D>
 __global__ __launch_bounds__(64) void merge_kernel(AttnArgs a, DecodePlan p) {
-  using E = typename Tr<DT>::Elem;
+  using E = typename Tr<DT>::QElem;
   const int j = blockIdx.x;
   const int h = blockIdx.y;
   if (j >= p.n_seqs) return;
@@ -508,7 +567,7 @@ __global__ __launch_bounds__(64) void merge_kernel(AttnArgs a, DecodePlan p) {
 // head); split x of token i of chunk j sits at slot item_base[j] + x*C + i.
 template <int DT, int D>
 __global__ __launch_bounds__(64) void prefill_merge_kernel(AttnArgs a, PrefillPlan p) {
-  using E = typename Tr<DT>::Elem;
+  using E = typename Tr<DT>::QElem;
   const int r = blockIdx.x;
   const int h = blockIdx.y;
   if (r >= p.row_start[p.n_seqs]) return;
@@ -531,7 +590,7 @@ __global__ __launch_bounds__(64) void prefill_merge_kernel(AttnArgs a, PrefillPl
 template <int DT, int D>
 __global__ __launch_bounds__(256) void prefill_kernel(AttnArgs a, PrefillPlan p) {
   using T = Tr<DT>;
-  using E = typename T::Elem;
+  using QE = typename T::QElem;
   constexpr int X = T::X;
   constexpr int R = D / (4 * X);
   constexpr int MT = D / 16;
@@ -559,10 +618,10 @@ __global__ __launch_bounds__(256) void prefill_kernel(AttnArgs a, PrefillPlan p)
   const int last_tok = min(first_tok + (wave * 16 + 15) / G, C - 1);
   const int kend = P + last_tok + 1;  // keys this wave needs
 
-  const E* q = reinterpret_cast<const E*>(a.q) + ((size_t)(t0 + i) * a.hq + h) * D;
+  const QE* q = reinterpret_cast<const QE*>(a.q) + ((size_t)(t0 + i) * a.hq + h) * D;
   typename T::Chunk qf[R];
 #pragma unroll
-  for (int r = 0; r < R; ++r) qf[r] = T::load_chunk(q + (4 * r + grp) * X);
+  for (int r = 0; r < R; ++r) qf[r] = T::load_q(q + (4 * r + grp) * X);
 
   RowState<DT, D> st;
 #pragma unroll
@@ -577,8 +636,8 @@ __global__ __launch_bounds__(256) void prefill_kernel(AttnArgs a, PrefillPlan p)
   float l = st.l + __shfl_xor(st.l, 16);
   l += __shfl_xor(l, 32);
   if (!row_ok) return;
-  const float inv = poison ? NAN : 1.f / l;
-  E* o = reinterpret_cast<E*>(a.out) + ((size_t)(t0 + i) * a.hq + h) * D;
+  const float inv = poison ? NAN : a.v_scale / l;
+  QE* o = reinterpret_cast<QE*>(a.out) + ((size_t)(t0 + i) * a.hq + h) * D;
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) T::store4(o + 16 * mt + 4 * grp, st.acc[mt] * inv);
   if (a.lse && grp == 0)
@@ -922,6 +981,26 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a, AppendPlan p)
   if (blk < 0 || blk >= a.nb) return;
   const int slot = pos % kBlock;
   const int nchunk = a.hkv * NC;
+  if constexpr (DT == 2) {
+    // fp8 cache: each bf16 element of the new rows is stored as the E4M3
+    // code of x * (1 / scale); a lane handles 8 consecutive elements
+    const uint16_t* kn = reinterpret_cast<const uint16_t*>(a.k_new) + (size_t)t * a.hkv * D;
+    const uint16_t* vn = reinterpret_cast<const uint16_t*>(a.v_new) + (size_t)t * a.hkv * D;
+    for (int ci = lane; ci < nchunk; ci += 64) {
+      const int h = ci / NC, c = ci - h * NC;
+      const size_t head = (size_t)blk * a.hkv + h;
+      float kx[8], vx[8];
+      Tr<0>::unpack(*reinterpret_cast<const u32x4*>(kn + h * D + c * 8), kx);
+      Tr<0>::unpack(*reinterpret_cast<const u32x4*>(vn + h * D + c * 8), vx);
+      u32x2 kc = {0u, 0u};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) kc[e / 4] |= f32_to_e4m3(kx[e] * a.inv_k_scale) << (8 * (e % 4));
+      *reinterpret_cast<u32x2*>(reinterpret_cast<uint8_t*>(a.k_cache) + ((head * NC + c) * kBlock + slot) * 8) = kc;
+      uint8_t* vc = reinterpret_cast<uint8_t*>(a.v_cache) + (head * D + c * 8) * kBlock + slot;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) vc[e * kBlock] = (uint8_t)f32_to_e4m3(vx[e] * a.inv_v_scale);
+    }
+  } else {
   for (int c0 = 0; c0 < nchunk; c0 += 64 * U) {
     u32x4 kv[U];
     E vv[U][X];
@@ -945,6 +1024,7 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a, AppendPlan p)
 #pragma unroll
       for (int e = 0; e < X; ++e) vc[e * kBlock] = vv[u][e];
     }
+  }
   }
 }
 
@@ -1033,6 +1113,8 @@ hipError_t dispatch(int dtype, int head_dim, Args&&... args) {
   if (dtype == 0 && head_dim == 64) return F<0, 64>::run(args...);
   if (dtype == 1 && head_dim == 128) return F<1, 128>::run(args...);
   if (dtype == 1 && head_dim == 64) return F<1, 64>::run(args...);
+  if (dtype == 2 && head_dim == 128) return F<2, 128>::run(args...);
+  if (dtype == 2 && head_dim == 64) return F<2, 64>::run(args...);
   return hipErrorInvalidValue;
 }
 
@@ -1050,11 +1132,15 @@ struct AppendL {
 template <int DT, int D>
 struct RopeAppendL {
   static hipError_t run(const AppendArgs& a, const AppendPlan& p, const RopeArgs& r, hipStream_t stream) {
-    const int tokens = p.tok_start[p.n_seqs];
-    if (tokens == 0) return hipSuccess;
-    hipLaunchKernelGGL((rope_append_kernel<DT, D>), dim3((tokens + kWavesPerGroup - 1) / kWavesPerGroup),
-                       dim3(64 * kWavesPerGroup), 0, stream, a, p, r);
-    return hipGetLastError();
+    if constexpr (DT == 2) {
+      return hipErrorInvalidValue;  // not built for fp8 caches (the host rejects it first)
+    } else {
+      const int tokens = p.tok_start[p.n_seqs];
+      if (tokens == 0) return hipSuccess;
+      hipLaunchKernelGGL((rope_append_kernel<DT, D>), dim3((tokens + kWavesPerGroup - 1) / kWavesPerGroup),
+                         dim3(64 * kWavesPerGroup), 0, stream, a, p, r);
+      return hipGetLastError();
+    }
   }
 };
 
@@ -1136,10 +1222,10 @@ int decode_wave_slots(int dtype, int head_dim) {
   // Concurrent decode waves the device can hold: workgroups per CU at this
   // kernel's register use, times waves per workgroup, times CUs.  Cached per
   // device; 2048 when there is no device to ask.
-  static std::atomic<int> cache[64][2][2];
+  static std::atomic<int> cache[64][3][2];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 2048;
-  const int di = dtype == 0 ? 0 : 1, hi = head_dim == 128 ? 0 : 1;
+  const int di = dtype == 0 ? 0 : dtype == 1 ? 1 : 2, hi = head_dim == 128 ? 0 : 1;
   const int known = cache[dev][di][hi].load(std::memory_order_relaxed);
   if (known > 0) return known;
   int cus = 0, per_cu = 0;
@@ -1153,6 +1239,10 @@ int decode_wave_slots(int dtype, int head_dim) {
     e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_kernel<1, 128>, 256, 0);
   else if (dtype == 1 && head_dim == 64)
     e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_kernel<1, 64>, 256, 0);
+  else if (dtype == 2 && head_dim == 128)
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_kernel<2, 128>, 256, 0);
+  else if (dtype == 2 && head_dim == 64)
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_kernel<2, 64>, 256, 0);
   if (e != hipSuccess || per_cu <= 0) return 2048;
   const int slots = per_cu * kWavesPerGroup * cus;
   cache[dev][di][hi].store(slots, std::memory_order_relaxed);

@@ -26,8 +26,8 @@ from workloads.device import device_step, host_subbatch, tensor_to_raw, to_devic
 
 pytestmark = pytest.mark.gpu
 
-TOL = {"bf16": (1e-2, 1e-3), "f32": (1e-4, 1e-5)}
-LSE_TOL = {"bf16": 2e-3, "f32": 1e-4}
+TOL = {"bf16": (1e-2, 1e-3), "f32": (1e-4, 1e-5), "fp8": (1e-2, 1e-3)}  # fp8: bf16 outputs
+LSE_TOL = {"bf16": 2e-3, "f32": 1e-4, "fp8": 2e-3}
 
 
 @pytest.fixture(scope="module")
@@ -50,13 +50,14 @@ def run_step(d, lse=True, append=True):
 
     if append:
         mpa.kv_append(d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
-                      d.seq_lens_host, d.qsl_host, block_tables_host=d.block_tables_host)
+                      d.seq_lens_host, d.qsl_host, block_tables_host=d.block_tables_host, k_scale=d.k_scale,
+                      v_scale=d.v_scale)
     out = torch.full_like(d.q, float("nan"))
     l = torch.full(d.q.shape[:2], float("nan"), dtype=torch.float32, device=d.q.device) if lse else None
     ws = mpa.alloc_workspace(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.qsl_host, d.scale)
     mpa.mixed_paged_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
                               d.seq_lens_host, d.qsl_host, out, lse=l, workspace=ws, scale=d.scale,
-                              block_tables_host=d.block_tables_host)
+                              block_tables_host=d.block_tables_host, k_scale=d.k_scale, v_scale=d.v_scale)
     torch.cuda.synchronize()
     return out, l
 
@@ -71,7 +72,8 @@ def bf16_to_f32(bits):
 
 def oracle_for(b):
     return ref.attention_reference(b.q, b.k_cache, b.v_cache, b.k_new, b.v_new, b.block_tables, b.seq_lens,
-                                   b.query_start_loc, b.scale, b.heads.num_kv_heads, b.heads.block_size, b.dtype)
+                                   b.query_start_loc, b.scale, b.heads.num_kv_heads, b.heads.block_size, b.dtype,
+                                   k_scale=b.k_scale, v_scale=b.v_scale)
 
 
 def assert_close(got, exp, dtype, what=""):
@@ -88,7 +90,8 @@ def check_batch(b, what):
     d = to_device(b)
     out, lse = run_step(d)
     kc, vc = ref.append_reference(b.k_cache, b.v_cache, b.k_new, b.v_new, b.block_tables, b.seq_lens,
-                                  b.query_start_loc, b.heads.block_size, b.dtype)
+                                  b.query_start_loc, b.heads.block_size, b.dtype, k_scale=b.k_scale,
+                                  v_scale=b.v_scale)
     assert tensor_to_raw(d.k_cache, b.dtype).tobytes() == kc.tobytes(), f"{what}: K append not bit-exact"
     assert tensor_to_raw(d.v_cache, b.dtype).tobytes() == vc.tobytes(), f"{what}: V append not bit-exact"
     o_ref, l_ref = oracle_for(b)
@@ -103,7 +106,7 @@ def check_batch(b, what):
 # small configurations, whole-batch parity
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dtype", ["bf16", "f32", "fp8"])
 @pytest.mark.parametrize("seed", [0, 1, 2, 3, 4])
 def test_tiny_config(torch_gpu, dtype, seed):
     check_batch(config_batch("tiny", seed, dtype), f"tiny seed={seed}")
@@ -130,7 +133,7 @@ def mixed_specs(rng):
 
 
 @pytest.mark.parametrize("heads", MIXES, ids=lambda h: f"hq{h[0]}_hkv{h[1]}_d{h[2]}")
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dtype", ["bf16", "f32", "fp8"])
 def test_mixed_batches(torch_gpu, heads, dtype):
     rng = np.random.default_rng(hash(heads) % 1000)
     specs = mixed_specs(rng)
@@ -257,6 +260,47 @@ def test_context_one_returns_v_exactly(torch_gpu):
         got = tensor_to_raw(out, dtype)
         for h in range(16):
             assert got[:, h].tobytes() == v[:, h // 4].tobytes()
+
+
+def test_fp8_context_one_returns_scaled_code_exactly(torch_gpu):
+    """Context-1 rows over an fp8 cache return code value * v_scale rounded
+    once to bf16, for every finite E4M3 code but -0 (whose sign an
+    accumulation from +0 drops): this pins the device's code table and where
+    the value scale enters."""
+    vals = ref.e4m3_values()
+    finite = np.array([c for c in range(256) if np.isfinite(vals[c]) and c != 0x80])
+    b = make_batch([SeqSpec(1, 1)] * 5, HeadSpec(16, 4, 128), "fp8", 24)
+    codes = np.resize(np.random.default_rng(24).permutation(finite), b.v_new.size)
+    b.v_new[:] = bf16_bits_from_f32((vals[codes] * b.v_scale).astype(np.float32)).reshape(b.v_new.shape)
+    assert np.array_equal(ref.fp8_codes(b.v_new, b.v_scale).ravel(), codes)  # the append keeps each code
+    d = to_device(b)
+    out, _ = run_step(d)
+    got = tensor_to_raw(out, "bf16")
+    expect = bf16_bits_from_f32(vals[codes].astype(np.float32) * np.float32(b.v_scale)).reshape(b.v_new.shape)
+    for h in range(16):
+        assert got[:, h].tobytes() == expect[:, h // 4].tobytes(), f"head {h}"
+
+
+def test_fp8_append_rounding_edges(torch_gpu):
+    """The fp8 append's rounding against the oracle on the format's edges
+    (unit scales, so that x * (1/scale) is x): ties to the even mantissa in
+    the normal and subnormal ranges and at the seam between them, the
+    saturation threshold 464, huge values, underflow with its sign, NaN."""
+    edges = np.array([1 + 1 / 16, 1 + 3 / 16, -(1 + 5 / 16), 7.5 * 2 ** -9, 0.5 * 2 ** -9, 1.5 * 2 ** -9,
+                      2.5 * 2 ** -9, 448, 456, 464, 480, 1e6, -1e6, -2 ** -12, 2 ** -11, 0.0, np.nan, 3.0,
+                      0.1, -0.3], np.float32)
+    b = make_batch([SeqSpec(20, 20), SeqSpec(7, 1)], HeadSpec(4, 2, 64), "fp8", 25)
+    b.k_scale = b.v_scale = 1.0
+    rng = np.random.default_rng(25)
+    for arr in (b.k_new, b.v_new):
+        arr[:] = bf16_bits_from_f32(rng.choice(edges, size=arr.shape).astype(np.float32))
+    d = to_device(b)
+    mpa.kv_append(d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
+                  d.seq_lens_host, d.qsl_host, k_scale=1.0, v_scale=1.0)
+    kc, vc = ref.append_reference(b.k_cache, b.v_cache, b.k_new, b.v_new, b.block_tables, b.seq_lens,
+                                  b.query_start_loc, 16, "fp8", k_scale=1.0, v_scale=1.0)
+    assert tensor_to_raw(d.k_cache, "fp8").tobytes() == kc.tobytes()
+    assert tensor_to_raw(d.v_cache, "fp8").tobytes() == vc.tobytes()
 
 
 def test_block_permutation_bit_identical(torch_gpu):
@@ -395,9 +439,13 @@ def oracle_rows(b, s, rows):
     L = int(b.seq_lens[s])
     P = L - c
     kp, vp = ref.gather_kv(b.k_cache, b.v_cache, b.block_tables[s], P, hkv, d, b.heads.block_size, b.dtype)
-    k = np.concatenate([kp, ref.decode_raw(b.k_new[t0:t0 + c], b.dtype)])
-    v = np.concatenate([vp, ref.decode_raw(b.v_new[t0:t0 + c], b.dtype)])
-    q = ref.decode_raw(b.q[t0:t0 + c], b.dtype)
+    if b.dtype == "fp8":  # codes * scale, the new rows as the append stores them
+        k = np.concatenate([kp, ref.decode_raw(ref.fp8_codes(b.k_new[t0:t0 + c], b.k_scale), "fp8")]) * b.k_scale
+        v = np.concatenate([vp, ref.decode_raw(ref.fp8_codes(b.v_new[t0:t0 + c], b.v_scale), "fp8")]) * b.v_scale
+    else:
+        k = np.concatenate([kp, ref.decode_raw(b.k_new[t0:t0 + c], b.dtype)])
+        v = np.concatenate([vp, ref.decode_raw(b.v_new[t0:t0 + c], b.dtype)])
+    q = ref.decode_raw(b.q[t0:t0 + c], b.qdtype)
     rows = np.asarray(rows)
     vis = np.arange(L)[None, :] <= (P + rows)[:, None]
     kh = [np.ascontiguousarray(k[:, g]) for g in range(hkv)]
@@ -413,14 +461,15 @@ def oracle_rows(b, s, rows):
 FULL = ["decode8b", "lent", "agentic", "budget0", "budget256", "budget1024", "budget4096", "longctx"]
 
 
-@pytest.mark.parametrize("name", FULL)
-def test_full_size_sampled(torch_gpu, name):
+@pytest.mark.parametrize("name,dtype", [(n, "bf16") for n in FULL] + [("decode8b", "fp8"), ("lent", "fp8")],
+                         ids=lambda x: x if isinstance(x, str) else None)
+def test_full_size_sampled(torch_gpu, name, dtype):
     import torch
 
     seed = 0
     specs, heads, nb, rng = config_specs(name, seed)
-    say(f"[gpu] full size {name}: {len(specs)} seqs, T={sum(s.q_len for s in specs)}")
-    d = device_step(specs, heads, "bf16", rng, seed, num_blocks=nb)
+    say(f"[gpu] full size {name} {dtype}: {len(specs)} seqs, T={sum(s.q_len for s in specs)}")
+    d = device_step(specs, heads, dtype, rng, seed, num_blocks=nb)
     srng = np.random.default_rng(1000 + seed)
     dec = [i for i, s in enumerate(specs) if s.q_len == 1]
     pre = [i for i, s in enumerate(specs) if s.q_len > 1]

@@ -15,7 +15,7 @@ from typing import Dict, List, Optional, Sequence
 
 import numpy as np
 
-from .gen import Batch, HeadSpec, SeqSpec, allocate_blocks, k_cache_shape, v_cache_shape
+from .gen import FP8_K_SCALE, FP8_V_SCALE, Batch, HeadSpec, SeqSpec, allocate_blocks, k_cache_shape, v_cache_shape
 
 
 def _torch():
@@ -26,11 +26,13 @@ def _torch():
 
 def _tdtype(dtype: str):
     torch = _torch()
-    return torch.bfloat16 if dtype == "bf16" else torch.float32
+    return {"bf16": torch.bfloat16, "fp8": torch.uint8}.get(dtype, torch.float32)
 
 
 def raw_to_tensor(raw: np.ndarray, dtype: str, device):
     torch = _torch()
+    if dtype == "fp8":
+        return torch.from_numpy(np.ascontiguousarray(raw, dtype=np.uint8)).to(device)
     if dtype == "bf16":
         t = torch.from_numpy(np.ascontiguousarray(raw).view(np.int16)).view(torch.bfloat16)
     else:
@@ -41,6 +43,8 @@ def raw_to_tensor(raw: np.ndarray, dtype: str, device):
 def tensor_to_raw(t, dtype: str) -> np.ndarray:
     torch = _torch()
     t = t.detach().contiguous().cpu()
+    if dtype == "fp8":
+        return t.view(torch.uint8).numpy().copy()
     if dtype == "bf16":
         return t.view(torch.int16).numpy().view(np.uint16).copy()
     return t.numpy().astype(np.float32, copy=True)
@@ -65,6 +69,12 @@ class DeviceStep:
     block_tables_host: np.ndarray
     seq_lens_host: np.ndarray
     qsl_host: np.ndarray
+    k_scale: float = 1.0
+    v_scale: float = 1.0
+
+    @property
+    def qdtype(self) -> str:
+        return "bf16" if self.dtype == "fp8" else self.dtype
 
     @property
     def total_q(self) -> int:
@@ -83,9 +93,9 @@ def to_device(b: Batch, device="cuda") -> DeviceStep:
         heads=b.heads,
         num_blocks=b.num_blocks,
         scale=b.scale,
-        q=raw_to_tensor(b.q, b.dtype, device),
-        k_new=raw_to_tensor(b.k_new, b.dtype, device),
-        v_new=raw_to_tensor(b.v_new, b.dtype, device),
+        q=raw_to_tensor(b.q, b.qdtype, device),
+        k_new=raw_to_tensor(b.k_new, b.qdtype, device),
+        v_new=raw_to_tensor(b.v_new, b.qdtype, device),
         k_cache=raw_to_tensor(b.k_cache, b.dtype, device),
         v_cache=raw_to_tensor(b.v_cache, b.dtype, device),
         block_tables=i32(b.block_tables),
@@ -94,16 +104,24 @@ def to_device(b: Batch, device="cuda") -> DeviceStep:
         block_tables_host=np.ascontiguousarray(b.block_tables, dtype=np.int32),
         seq_lens_host=np.ascontiguousarray(b.seq_lens, dtype=np.int32),
         qsl_host=np.ascontiguousarray(b.query_start_loc, dtype=np.int32),
+        k_scale=b.k_scale,
+        v_scale=b.v_scale,
     )
 
 
-def _randn_into(t, gen, chunk_elems: int = 1 << 28):
-    """Fill a tensor with N(0,1) drawn in float32 and rounded to its dtype."""
+def _randn_into(t, gen, chunk_elems: int = 1 << 28, fp8_scale: float = 1.0):
+    """Fill a tensor with N(0,1) drawn in float32 and rounded to its dtype (a
+    uint8 tensor receives the E4M3 codes of the values over fp8_scale, via
+    torch's float8_e4m3fn conversion after clipping to +-448)."""
     torch = _torch()
     flat = t.view(-1)
     for i in range(0, flat.numel(), chunk_elems):
         n = min(chunk_elems, flat.numel() - i)
-        flat[i : i + n] = torch.randn(n, generator=gen, device=t.device, dtype=torch.float32).to(t.dtype)
+        x = torch.randn(n, generator=gen, device=t.device, dtype=torch.float32)
+        if t.dtype == torch.uint8:
+            flat[i : i + n] = (x / fp8_scale).clamp_(-448.0, 448.0).to(torch.float8_e4m3fn).view(torch.uint8)
+        else:
+            flat[i : i + n] = x.to(t.dtype)
 
 
 def device_step(
@@ -126,15 +144,19 @@ def device_step(
     qsl[1:] = np.cumsum([s.q_len for s in specs])
     t = int(qsl[-1])
     td = _tdtype(dtype)
+    tq = _tdtype("bf16" if dtype == "fp8" else dtype)
+    ks, vs = (FP8_K_SCALE, FP8_V_SCALE) if dtype == "fp8" else (1.0, 1.0)
     gen = torch.Generator(device=device)
     gen.manual_seed(int(seed))
-    q = torch.empty((t, heads.num_q_heads, heads.head_dim), dtype=td, device=device)
-    k_new = torch.empty((t, heads.num_kv_heads, heads.head_dim), dtype=td, device=device)
+    q = torch.empty((t, heads.num_q_heads, heads.head_dim), dtype=tq, device=device)
+    k_new = torch.empty((t, heads.num_kv_heads, heads.head_dim), dtype=tq, device=device)
     v_new = torch.empty_like(k_new)
     k_cache = torch.empty(k_cache_shape(num_blocks, heads, dtype), dtype=td, device=device)
     v_cache = torch.empty(v_cache_shape(num_blocks, heads, dtype), dtype=td, device=device)
-    for x in (q, k_new, v_new, k_cache, v_cache):
+    for x in (q, k_new, v_new):
         _randn_into(x, gen)
+    _randn_into(k_cache, gen, fp8_scale=ks)
+    _randn_into(v_cache, gen, fp8_scale=vs)
     # NaN sentinels
     bs = heads.block_size
     used = np.zeros(num_blocks, dtype=bool)
@@ -146,7 +168,7 @@ def device_step(
         pos = np.arange(s.ctx - s.q_len, n * bs)
         blk_idx.append(bt[i, pos // bs])
         slot_idx.append(pos % bs)
-    nan = float("nan")
+    nan = 0x7F if dtype == "fp8" else float("nan")
     unused = torch.from_numpy(np.nonzero(~used)[0]).to(device)
     if unused.numel():
         k_cache[unused] = nan
@@ -173,6 +195,8 @@ def device_step(
         block_tables_host=np.ascontiguousarray(bt, dtype=np.int32),
         seq_lens_host=seq_lens,
         qsl_host=qsl,
+        k_scale=ks,
+        v_scale=vs,
     )
 
 
@@ -212,11 +236,13 @@ def host_subbatch(d: DeviceStep, seqs: Sequence[int]) -> Dict:
         seq_lens=np.array(lens, dtype=np.int32),
         query_start_loc=qsl,
         block_tables=bt,
-        q=tensor_to_raw(d.q.index_select(0, ridx), d.dtype),
-        k_new=tensor_to_raw(d.k_new.index_select(0, ridx), d.dtype),
-        v_new=tensor_to_raw(d.v_new.index_select(0, ridx), d.dtype),
+        q=tensor_to_raw(d.q.index_select(0, ridx), d.qdtype),
+        k_new=tensor_to_raw(d.k_new.index_select(0, ridx), d.qdtype),
+        v_new=tensor_to_raw(d.v_new.index_select(0, ridx), d.qdtype),
         k_cache=kc,
         v_cache=vc,
         scale=d.scale,
+        k_scale=d.k_scale,
+        v_scale=d.v_scale,
     )
     return {"batch": sub, "rows": rows_all}

@@ -15,8 +15,13 @@ slot that the step must not read before its own append -- unreferenced blocks,
 the slots this step appends to, and the slots past ``ctx`` in a sequence's last
 block -- holds NaN, so a kernel that reads one shows it in its output.
 
+dtype "fp8" is an fp8 KV cache (OCP E4M3 codes, one scale per tensor) next to
+bf16 queries and new rows: the pool's values are N(0, 1) divided by the
+tensor's scale and mapped to the nearest code (the sentinel is the NaN code
+0x7F).
+
 Cache layout (the one ``include/mpa.h`` defines; the paper is silent on it),
-with ``X = 16 / element_bytes`` (8 for bf16, 4 for fp32):
+with ``X`` elements per K chunk (8 for bf16 and fp8, 4 for fp32):
 
 * K: ``[num_blocks][num_kv_heads][head_dim / X][block_size][X]``
 * V: ``[num_blocks][num_kv_heads][head_dim][block_size]``
@@ -30,9 +35,15 @@ from typing import List, Optional, Sequence
 
 import numpy as np
 
-ELEM_BYTES = {"bf16": 2, "f32": 4}
-RAW_DTYPE = {"bf16": np.uint16, "f32": np.float32}
+ELEM_BYTES = {"bf16": 2, "f32": 4, "fp8": 1}
+RAW_DTYPE = {"bf16": np.uint16, "f32": np.float32, "fp8": np.uint8}
+CHUNK = {"bf16": 8, "f32": 4, "fp8": 8}
 BF16_NAN = np.uint16(0x7FC0)
+FP8_NAN = np.uint8(0x7F)
+# per-tensor scales of the fp8 pools: the largest code (448) covers 6.3 and
+# 7.5 standard deviations of the N(0, 1) values
+FP8_K_SCALE = 0.0141
+FP8_V_SCALE = 0.0167
 
 
 @dataclass(frozen=True)
@@ -50,7 +61,7 @@ class HeadSpec:
 
 
 def _x(dtype: str) -> int:
-    return 16 // ELEM_BYTES[dtype]
+    return CHUNK[dtype]
 
 
 def k_cache_shape(num_blocks: int, heads: HeadSpec, dtype: str):
@@ -72,10 +83,25 @@ def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
     return r
 
 
-def _draw_values(rng: np.random.Generator, shape, dtype: str) -> np.ndarray:
+def _fp8_nearest_codes(x: np.ndarray) -> np.ndarray:
+    """Input drawing only: the E4M3 code nearest to each value (the sign
+    kept, magnitudes clipped to 448); how ties break does not matter here."""
+    codes = np.arange(0x7F)
+    e, m = codes >> 3, codes & 7
+    vals = np.where(e == 0, m * 2.0 ** -9, (1 + m / 8.0) * 2.0 ** (e - 7.0))
+    a = np.minimum(np.abs(x.astype(np.float64)), 448.0)
+    hi = np.clip(np.searchsorted(vals, a), 0, 0x7E)
+    lo = np.clip(hi - 1, 0, 0x7E)
+    pick = np.where(a - vals[lo] <= vals[hi] - a, lo, hi)
+    return (pick | np.where(x < 0, 0x80, 0)).astype(np.uint8)
+
+
+def _draw_values(rng: np.random.Generator, shape, dtype: str, fp8_scale: float = 1.0) -> np.ndarray:
     v = rng.standard_normal(size=shape, dtype=np.float32)
     if dtype == "bf16":
         return bf16_bits_from_f32(v)
+    if dtype == "fp8":
+        return _fp8_nearest_codes(v / np.float32(fp8_scale))
     return v
 
 
@@ -96,6 +122,13 @@ class Batch:
     v_cache: np.ndarray  # raw, V layout above, contents before the append
     scale: float
     seed: Optional[int] = None
+    k_scale: float = 1.0  # fp8 caches: value = code value * scale
+    v_scale: float = 1.0
+
+    @property
+    def qdtype(self) -> str:
+        """Storage of q, k_new, v_new and the outputs."""
+        return "bf16" if self.dtype == "fp8" else self.dtype
 
     @property
     def num_seqs(self) -> int:
@@ -141,7 +174,7 @@ def allocate_blocks(
 
 def _nan_fill(k_cache, v_cache, block_tables, specs, heads: HeadSpec, dtype: str):
     bs = heads.block_size
-    nan = BF16_NAN if dtype == "bf16" else np.float32(np.nan)
+    nan = {"bf16": BF16_NAN, "fp8": FP8_NAN}.get(dtype, np.float32(np.nan))
     used = np.zeros(k_cache.shape[0], dtype=bool)
     for i, s in enumerate(specs):
         n = -(-s.ctx // bs) if s.ctx > 0 else 0
@@ -183,11 +216,13 @@ def make_batch(
     qsl = np.zeros(len(specs) + 1, dtype=np.int32)
     qsl[1:] = np.cumsum([s.q_len for s in specs])
     t = int(qsl[-1])
-    q = _draw_values(rng, (t, heads.num_q_heads, heads.head_dim), dtype)
-    k_new = _draw_values(rng, (t, heads.num_kv_heads, heads.head_dim), dtype)
-    v_new = _draw_values(rng, (t, heads.num_kv_heads, heads.head_dim), dtype)
-    k_cache = _draw_values(rng, k_cache_shape(num_blocks, heads, dtype), dtype)
-    v_cache = _draw_values(rng, v_cache_shape(num_blocks, heads, dtype), dtype)
+    qd = "bf16" if dtype == "fp8" else dtype
+    ks, vs = (FP8_K_SCALE, FP8_V_SCALE) if dtype == "fp8" else (1.0, 1.0)
+    q = _draw_values(rng, (t, heads.num_q_heads, heads.head_dim), qd)
+    k_new = _draw_values(rng, (t, heads.num_kv_heads, heads.head_dim), qd)
+    v_new = _draw_values(rng, (t, heads.num_kv_heads, heads.head_dim), qd)
+    k_cache = _draw_values(rng, k_cache_shape(num_blocks, heads, dtype), dtype, ks)
+    v_cache = _draw_values(rng, v_cache_shape(num_blocks, heads, dtype), dtype, vs)
     if nan_fill:
         _nan_fill(k_cache, v_cache, bt, specs, heads, dtype)
     if scale is None:
@@ -206,6 +241,8 @@ def make_batch(
         v_cache=v_cache,
         scale=float(scale),
         seed=seed,
+        k_scale=ks,
+        v_scale=vs,
     )
 
 
