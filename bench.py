@@ -60,15 +60,18 @@ WORKLOADS = {
 }
 
 
-def algorithmic_work(seq_lens, qsl, hq, hkv, d, elem_bytes, block=16):
-    """Bytes and FLOPs the step must move / compute at minimum.
+def algorithmic_work(seq_lens, qsl, hq, hkv, d, elem_bytes, block=16, kv_bytes=None):
+    """Bytes and FLOPs the step must move / compute at minimum, with e the
+    bytes of a query / output element and c those of a cache element (c = e
+    unless the cache is fp8):
 
-    decode row (context L):   K+V read 2*L*Hkv*d*e, q read + out write
+    decode row (context L):   K+V read 2*L*Hkv*d*c, q read + out write
                               2*Hq*d*e, block ids 4*ceil(L/16)
-    prefill chunk (C on P):   K+V read 2*(P+C)*Hkv*d*e, q + out 2*C*Hq*d*e
-    append:                   new K/V read and written, 4*T*Hkv*d*e
+    prefill chunk (C on P):   K+V read 2*(P+C)*Hkv*d*c, q + out 2*C*Hq*d*e
+    append:                   new K/V read 2*T*Hkv*d*e, written 2*T*Hkv*d*c
     FLOPs: 4*d*Hq per attended (query, key) pair; decode attends L pairs,
     a chunk C*P + C*(C+1)/2."""
+    c = elem_bytes if kv_bytes is None else kv_bytes
     seq_lens = np.asarray(seq_lens, dtype=np.int64)
     q_lens = np.diff(np.asarray(qsl, dtype=np.int64))
     dec = q_lens == 1
@@ -76,9 +79,9 @@ def algorithmic_work(seq_lens, qsl, hq, hkv, d, elem_bytes, block=16):
     L = seq_lens
     P = L - q_lens
     C = q_lens
-    dec_bytes = int(np.sum((2 * L * hkv * d * elem_bytes + 2 * hq * d * elem_bytes + 4 * ((L + block - 1) // block))[dec]))
-    pre_bytes = int(np.sum((2 * L * hkv * d * elem_bytes + 2 * C * hq * d * elem_bytes)[pre]))
-    app_bytes = int(4 * q_lens.sum() * hkv * d * elem_bytes)
+    dec_bytes = int(np.sum((2 * L * hkv * d * c + 2 * hq * d * elem_bytes + 4 * ((L + block - 1) // block))[dec]))
+    pre_bytes = int(np.sum((2 * L * hkv * d * c + 2 * C * hq * d * elem_bytes)[pre]))
+    app_bytes = int(2 * q_lens.sum() * hkv * d * (elem_bytes + c))
     dec_flops = int(4 * d * hq * np.sum(L[dec]))
     pre_flops = int(4 * d * hq * np.sum((C * P + C * (C + 1) // 2)[pre]))
     return {
@@ -168,9 +171,13 @@ def cpu_baseline(d, budget_s: float, seed: int):
             t0 = time.perf_counter()
             prefix = int(sub.seq_lens[0]) - c
             kp, vp = ref.gather_kv(sub.k_cache, sub.v_cache, sub.block_tables[0], prefix, hkv, hd, bs, sub.dtype)
-            k = np.concatenate([kp, ref.decode_raw(sub.k_new, sub.dtype)])
-            v = np.concatenate([vp, ref.decode_raw(sub.v_new, sub.dtype)])
-            ref.sequence_attention(ref.decode_raw(sub.q, sub.dtype), k, v, prefix, sub.scale, hkv, rows=rows)
+            if sub.dtype == "fp8":
+                k = np.concatenate([kp, ref.decode_raw(ref.fp8_codes(sub.k_new, sub.k_scale), "fp8")]) * sub.k_scale
+                v = np.concatenate([vp, ref.decode_raw(ref.fp8_codes(sub.v_new, sub.v_scale), "fp8")]) * sub.v_scale
+            else:
+                k = np.concatenate([kp, ref.decode_raw(sub.k_new, sub.dtype)])
+                v = np.concatenate([vp, ref.decode_raw(sub.v_new, sub.dtype)])
+            ref.sequence_attention(ref.decode_raw(sub.q, sub.qdtype), k, v, prefix, sub.scale, hkv, rows=rows)
             elapsed += time.perf_counter() - t0
             rows_done += len(rows)
             visits += 1
@@ -200,6 +207,9 @@ def main(argv=None) -> int:
     ap.add_argument("--streams", type=int, default=1, choices=(1, 2),
                     help="2: the decode and prefill halves of the step run concurrently on two streams "
                          "(the library's mpa_decode_attention / mpa_prefill_attention); 1 (default): one after the other")
+    ap.add_argument("--kv", default="bf16", choices=("bf16", "fp8"),
+                    help="KV-cache element type: bf16 (default) or fp8 (OCP E4M3 codes, one scale per cache; "
+                         "queries and outputs stay bf16)")
     ap.add_argument("--graph", action="store_true",
                     help="also capture one step into a HIP graph (torch.cuda.graph) and time its replays")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -230,8 +240,10 @@ def main(argv=None) -> int:
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     mpa.lib()
     specs, heads, nb, rng = config_specs(args.config, args.seed)
-    d = device_step(specs, heads, "bf16", rng, args.seed, num_blocks=nb)
-    work = algorithmic_work(d.seq_lens_host, d.qsl_host, heads.num_q_heads, heads.num_kv_heads, heads.head_dim, 2)
+    d = device_step(specs, heads, args.kv, rng, args.seed, num_blocks=nb)
+    work = algorithmic_work(d.seq_lens_host, d.qsl_host, heads.num_q_heads, heads.num_kv_heads, heads.head_dim, 2,
+                            kv_bytes=1 if args.kv == "fp8" else 2)
+    sc = dict(k_scale=d.k_scale, v_scale=d.v_scale)
     ws = mpa.alloc_workspace(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.qsl_host, d.scale)
     out = torch.empty_like(d.q)
     lse = torch.empty(d.q.shape[:2], dtype=torch.float32, device=d.q.device)
@@ -254,7 +266,7 @@ def main(argv=None) -> int:
 
         mark("start", stream)
         mpa.kv_append(d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
-                      d.seq_lens_host, d.qsl_host, stream=stream)
+                      d.seq_lens_host, d.qsl_host, stream=stream, **sc)
         mark("append", stream)
         pre_stream = stream
         if two:
@@ -263,12 +275,12 @@ def main(argv=None) -> int:
         if has_pre:
             mpa.prefill_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
                                   d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws, scale=d.scale,
-                                  stream=pre_stream)
+                                  stream=pre_stream, **sc)
         mark("prefill", pre_stream)
         if has_dec:
             mpa.decode_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
                                  d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws, scale=d.scale,
-                                 stream=stream)
+                                 stream=stream, **sc)
         mark("decode", stream)
         if two:
             stream.wait_stream(side)
@@ -316,14 +328,14 @@ def main(argv=None) -> int:
         kernel = "decode_kernel+merge_kernel"
     else:
         achieved, peak, unit, bound = pre_tflops, MFMA_BF16_PEAK_TFLOPS, "TFLOP/s", "mfma"
-        kernel = "prefill_mfma_kernel"
+        kernel = "prefill_mfma_kernel" if args.kv == "bf16" else "prefill_kernel"
     roofline = {
         "bound": bound,
         "achieved": round(achieved, 2),
         "peak": peak,
         "unit": unit,
         "frac": round(achieved / peak, 4),
-        "traffic": measured_traffic(args.config, dom),
+        "traffic": measured_traffic(args.config, dom) if args.kv == "bf16" else None,
         "kernel": kernel,
         "phase_ms": round(dom_ms, 4),
         "algorithmic_per_launch": work[f"{dom}_bytes"] if dom == "decode" else work["prefill_flops"],
@@ -344,6 +356,7 @@ def main(argv=None) -> int:
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) values, shuffled block tables)",
         "config": {"workload": f"{args.config}: {WORKLOADS[args.config]}", "seed": args.seed, "streams": args.streams if two else 1,
+                   "kv_cache": "bf16" if args.kv == "bf16" else "fp8 e4m3 (per-cache scale)",
                    "decode_rows": work["decode_rows"], "prefill_chunks": work["prefill_chunks"],
                    "query_tokens": work["query_tokens"], "parallelism": "single GPU"},
         "roofline": roofline,
@@ -363,11 +376,12 @@ def main(argv=None) -> int:
     line["step_roofline"] = {"t_mem_ms": round(t_mem * 1e3, 4), "t_mfma_ms": round(t_mfma * 1e3, 4),
                              "max_frac": round(max(t_mem, t_mfma) / t_step, 4),
                              "sum_frac": round((t_mem + t_mfma) / t_step, 4)}
-    # the library's step-time model (mpa_predict_step) for this batch
-    pred = mpa.predict_step(mpa.shape_of(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.scale),
-                            d.seq_lens_host, d.qsl_host)
-    line["model_ms"] = {"append": round(pred.append_us * 1e-3, 4), "decode": round(pred.decode_us * 1e-3, 4),
-                        "prefill": round(pred.prefill_us * 1e-3, 4), "step": round(pred.step_us * 1e-3, 4)}
+    # the library's step-time model (mpa_predict_step; bf16 caches) for this batch
+    if args.kv == "bf16":
+        pred = mpa.predict_step(mpa.shape_of(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.scale),
+                                d.seq_lens_host, d.qsl_host)
+        line["model_ms"] = {"append": round(pred.append_us * 1e-3, 4), "decode": round(pred.decode_us * 1e-3, 4),
+                            "prefill": round(pred.prefill_us * 1e-3, 4), "step": round(pred.step_us * 1e-3, 4)}
     if args.graph:
         # the same step (no events) recorded once and replayed: every launch
         # carries its plan as kernel arguments, so the graph is a fixed
