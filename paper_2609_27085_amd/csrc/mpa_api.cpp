@@ -113,10 +113,10 @@ long decode_items(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens, 
   return n;
 }
 
-// Query tokens per prefill tile: 256 (token, head) rows for the bf16 MFMA
-// kernel, 64 for the generic (f32) kernel.
+// Query tokens per prefill tile: 256 (token, head) rows for the MFMA kernel
+// (bf16 and fp8 caches), 64 for the generic kernel (f32).
 int q_tile(const mpa_shape* sh) {
-  const int rows = sh->dtype == MPA_BF16 ? mpa::kPrefillRowsMfma : mpa::kPrefillRows;
+  const int rows = sh->dtype == MPA_F32 ? mpa::kPrefillRows : mpa::kPrefillRowsMfma;
   return rows / (sh->num_q_heads / sh->num_kv_heads);
 }
 
@@ -148,7 +148,7 @@ struct PrefillSplit {
 std::vector<PrefillSplit> prefill_splits(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens,
                                          const int32_t* qsl, long first_item) {
   std::vector<PrefillSplit> out(b.prefill.size());
-  if (sh->dtype != MPA_BF16 || b.prefill.empty()) return out;
+  if (sh->dtype == MPA_F32 || b.prefill.empty()) return out;
   const int qt = q_tile(sh);
   long units = 0;
   for (int s : b.prefill) units += (long)(qsl[s + 1] - qsl[s] + qt - 1) / qt * sh->num_kv_heads;
@@ -539,12 +539,12 @@ int run_attention(int phases, const mpa_shape* shape, const void* q, const void*
       if (e != hipSuccess) return MPA_ERR_HIP;
     }
   }
-  // bf16: the MFMA kernel rounds every probability to bf16, which averages
+  // bf16 and fp8: the MFMA kernel rounds every probability to bf16, which averages
   // out over many keys but not over a handful.  The rows that see at most
   // kFewKeys keys (the first tokens of a chunk on a shorter prefix) are
   // recomputed, after it on the same stream, by the generic kernel, which
   // carries their probabilities to about 16 bits.
-  if (shape->dtype == MPA_BF16) {
+  if (shape->dtype != MPA_F32) {
     const int qg = mpa::kPrefillRows / (shape->num_q_heads / shape->num_kv_heads);
     std::vector<std::pair<int, int>> few;  // (sequence, tiles of qg tokens)
     for (int s : b.prefill) {

@@ -674,7 +674,7 @@ __global__ __launch_bounds__(256) void prefill_kernel(AttnArgs a, PrefillPlan p)
 // running reference m only moves when a row's new maximum exceeds it by more
 // than 8 (log2 units), so exp2(s - m) <= 2^8 and the O / l rescale is skipped
 // for almost every tile; the final O / l is the same quotient either way.
-template <int D, int WAVES, int STAGES>
+template <int CT, int D, int WAVES, int STAGES>
 __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a, PrefillPlan p) {
   using f32x16 = float __attribute__((ext_vector_type(16)));
   using cint = const __attribute__((address_space(4))) int32_t;
@@ -688,6 +688,14 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   constexpr int WI = NI / WAVES;           // ... per wave
   static_assert(WI >= 1 && NI % WAVES == 0 && (WI * 512) <= BLK && BLK % (WI * 512) == 0,
                 "each wave copies part of exactly one block per tile");
+  // CT: the cache type, 0 bf16 or 2 fp8.  fp8 codes take a register path:
+  // each lane loads one 16-byte piece of the K tile and one of the V tile
+  // (a (block, head) granule has D such pieces), one tile ahead, and at the
+  // end of the iteration converts them to bf16 into the same LDS layout the
+  // bf16 copies fill, so the compute below is the same for both.
+  static_assert(CT == 0 || CT == 2, "bf16 or fp8 caches");
+  static_assert(CT == 0 || (NB * D <= 64 * WAVES && (64 * WAVES) % D == 0), "one fp8 piece per lane");
+  constexpr int AHEAD = CT == 2 ? 1 : STAGES - 1;  // tiles a copy runs ahead of its use
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   uint16_t* const sk = smem;                   // STAGES K tiles
   uint16_t* const sv = smem + STAGES * TILE;   // STAGES V tiles
@@ -738,15 +746,26 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
 
   // ---- global -> LDS tile copies (this wave's slices)
   const int nblk = (kend + kBlock - 1) / kBlock;
-  const int my_bi = (wave * WI * 512) / BLK;  // the tile block this wave copies
+  const int pi = wave * 64 + lane;  // fp8: this lane's 16-byte piece of the tile
+  const int my_bi = CT == 2 ? (wave * 64) / D : (wave * WI * 512) / BLK;  // the tile block this wave copies
+  u32x4 kraw = {0u, 0u, 0u, 0u}, vraw = {0u, 0u, 0u, 0u};  // fp8 pieces in flight
   // Tile kt's copy.  A block index past the sequence's last needed block is
   // clamped to it (its keys are all masked and its V entries zeroed), so
   // every copy is issued, always 2*WI instructions per wave per tile.
   // the id of the block this wave copies for tile kt (a scalar load)
   auto tile_block = [&](int kt) -> int { return bt[min(kt * NB + my_bi, nblk - 1)]; };
   auto copy_tile = [&](int kt, int blk_raw) -> int {
-    const int stage = kt % STAGES;
     const int blk = (blk_raw >= 0 && blk_raw < a.nb) ? blk_raw : 0;
+    if constexpr (CT == 2) {
+      if (pi < NB * D) {
+        const size_t gran = ((size_t)blk * a.hkv + g) * (kBlock * D) + (size_t)(pi % D) * 16;
+        kraw = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint8_t*>(a.k_cache) + gran);
+        vraw = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint8_t*>(a.v_cache) + gran);
+      }
+      (void)kt;
+      return blk_raw;
+    }
+    const int stage = kt % STAGES;
     const size_t gran = ((size_t)blk * a.hkv + g) * BLK;
     const uint16_t* kbase = reinterpret_cast<const uint16_t*>(a.k_cache) + gran;
     const uint16_t* vbase = reinterpret_cast<const uint16_t*>(a.v_cache) + gran;
@@ -784,6 +803,43 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
         if (bad || e >= nvalid) piece[e] = bad ? (uint16_t)0x7FC0 : (uint16_t)0;
     }
   };
+  // fp8: once this lane's pieces of tile kt have landed, store them as bf16
+  // in the tile's stage -- K piece q (keys 2j, 2j+1 of chunk c = q/8, j = q%8)
+  // at the slots of those keys, V piece q (V^T row q, 16 keys) as its two key
+  // halves -- with the V entries of keys >= L zeroed (NaN for a bad block id)
+  auto store_fp8_tile = [&](int kt, int blk_raw) {
+    if (pi >= NB * D) return;
+    const int b = pi / D, q = pi % D;
+    uint8_t* kdst = reinterpret_cast<uint8_t*>(sk + (kt % STAGES) * TILE + b * BLK);
+    uint8_t* vdst = reinterpret_cast<uint8_t*>(sv + (kt % STAGES) * TILE + b * BLK);
+    const int c = q >> 3, j = q & 7;
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+      const int key = 2 * j + x;
+      const int slot = (key & 3) | ((key & 4) << 1) | ((key & 8) >> 1);  // the slot that holds this key
+      const u32x4 w = {Tr<2>::cvt2(kraw[2 * x], false), Tr<2>::cvt2(kraw[2 * x], true),
+                       Tr<2>::cvt2(kraw[2 * x + 1], false), Tr<2>::cvt2(kraw[2 * x + 1], true)};
+      *reinterpret_cast<u32x4*>(kdst + (c * 16 + slot) * 16) = w;
+    }
+    const int nvalid = L - (kt * NB + b) * kBlock;
+    const bool bad = !(blk_raw >= 0 && blk_raw < a.nb);
+#pragma unroll
+    for (int vh = 0; vh < 2; ++vh) {
+      u32x4 w = {Tr<2>::cvt2(vraw[2 * vh], false), Tr<2>::cvt2(vraw[2 * vh], true),
+                 Tr<2>::cvt2(vraw[2 * vh + 1], false), Tr<2>::cvt2(vraw[2 * vh + 1], true)};
+      if (bad || nvalid < 8 * vh + 8) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const unsigned keep = (unsigned)(!bad && 8 * vh + e < nvalid);
+          const unsigned fill = bad ? 0x7FC0u : 0u;
+          const unsigned sh = 16 * (e & 1);
+          const unsigned cur = (w[e >> 1] >> sh) & 0xFFFFu;
+          w[e >> 1] = (w[e >> 1] & ~(0xFFFFu << sh)) | ((keep ? cur : fill) << sh);
+        }
+      }
+      *reinterpret_cast<u32x4*>(vdst + (vh * D + q) * 16) = w;
+    }
+  };
 
   f32x16 o[DT];
 #pragma unroll
@@ -800,14 +856,19 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   // the Q fragments (ordinary loads) land before any tile copy is issued, so
   // that no wait inside the loop is ever needed for them
   MPA_WAIT_VMCNT(0);
-  // prologue: the split's first STAGES-1 tiles in flight, its first published
+  // prologue: the split's first AHEAD tiles in flight, its first published
   int blk_id[STAGES];
 #pragma unroll
-  for (int k = 0; k < STAGES - 1; ++k) blk_id[(kt_begin + k) % STAGES] = copy_tile(kt_begin + k, tile_block(kt_begin + k));
+  for (int k = 0; k < AHEAD; ++k) blk_id[(kt_begin + k) % STAGES] = copy_tile(kt_begin + k, tile_block(kt_begin + k));
   // each iteration loads the block id the next one copies (see below)
-  int next_blk = tile_block(kt_begin + STAGES - 1);
-  MPA_WAIT_VMCNT(2 * WI * (STAGES - 2));
-  fix_tile(kt_begin, blk_id[kt_begin % STAGES]);
+  int next_blk = tile_block(kt_begin + AHEAD);
+  if constexpr (CT == 2) {
+    MPA_WAIT_VMCNT(0);
+    store_fp8_tile(kt_begin, blk_id[kt_begin % STAGES]);
+  } else {
+    MPA_WAIT_VMCNT(2 * WI * (STAGES - 2));
+    fix_tile(kt_begin, blk_id[kt_begin % STAGES]);
+  }
   __syncthreads();
 
   // Waves w and w + WAVES/2 share a SIMD and run the same phases; the issue
@@ -820,7 +881,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
     // past it): by an active wave between its first QK products, so that the
     // copy instructions are issued while the matrix core is busy
     const int cblk = next_blk;
-    blk_id[(kt + STAGES - 1) % STAGES] = cblk;
+    blk_id[(kt + AHEAD) % STAGES] = cblk;
     const int key_base = kt * BN;
     if (wave_active && key_base < w_kend) {
       const uint16_t* K = sk + (kt % STAGES) * TILE;
@@ -850,7 +911,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
           st[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[rt][ks], qf[ks], st[rt], 0, 0, 0);
         if (ks == 1) {
           __builtin_amdgcn_sched_barrier(0);
-          copy_tile(kt + STAGES - 1, cblk);
+          copy_tile(kt + AHEAD, cblk);
           __builtin_amdgcn_sched_barrier(0);
         }
       }
@@ -867,7 +928,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
       // and may complete out of order, so issued here, after the last LDS
       // read of the tile, it only turns the PV waits into full ones, by
       // which time the V reads have long landed
-      next_blk = tile_block(kt + STAGES);
+      next_blk = tile_block(kt + AHEAD + 1);
       if (key_base + BN - 1 > w_min_limit) {
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
@@ -914,13 +975,19 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
         for (int dt = 0; dt < DT; ++dt) o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[t][dt], pb[t], o[dt], 0, 0, 0);
       l += (l4[0] + l4[1]) + (l4[2] + l4[3]);
     } else {
-      copy_tile(kt + STAGES - 1, cblk);
-      next_blk = tile_block(kt + STAGES);
+      copy_tile(kt + AHEAD, cblk);
+      next_blk = tile_block(kt + AHEAD + 1);
     }
-    // this wave's part of tile kt+1 has landed once only the copies issued
-    // after it (tiles kt+2 .. kt+STAGES-1) remain in flight
-    MPA_WAIT_VMCNT(2 * WI * (STAGES - 2));
-    fix_tile(kt + 1, blk_id[(kt + 1) % STAGES]);
+    if constexpr (CT == 2) {
+      // this lane's pieces of tile kt+1 (the only loads in flight)
+      MPA_WAIT_VMCNT(0);
+      store_fp8_tile(kt + 1, blk_id[(kt + 1) % STAGES]);
+    } else {
+      // this wave's part of tile kt+1 has landed once only the copies issued
+      // after it (tiles kt+2 .. kt+STAGES-1) remain in flight
+      MPA_WAIT_VMCNT(2 * WI * (STAGES - 2));
+      fix_tile(kt + 1, blk_id[(kt + 1) % STAGES]);
+    }
     __syncthreads();
   }
   MPA_WAIT_VMCNT(0);  // drain the clamped copies past the end
@@ -935,7 +1002,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
 #pragma unroll
       for (int jb = 0; jb < 4; ++jb) {
         const f32x4 v4 = {o[dt][4 * jb], o[dt][4 * jb + 1], o[dt][4 * jb + 2], o[dt][4 * jb + 3]};
-        *reinterpret_cast<f32x4*>(wo + 32 * dt + 8 * jb + 4 * h) = v4;
+        *reinterpret_cast<f32x4*>(wo + 32 * dt + 8 * jb + 4 * h) = v4 * a.v_scale;
       }
     if (h == 0) {
       a.ws_ml[slot * 2] = m_ref * c;
@@ -943,7 +1010,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
     }
     return;
   }
-  const float inv = 1.f / lt;
+  const float inv = a.v_scale / lt;
   uint16_t* out = reinterpret_cast<uint16_t*>(a.out) + ((size_t)(t0 + i) * a.hq + head) * D;
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt)
@@ -1167,10 +1234,10 @@ struct MergeL {
 constexpr int kPrefillWaves = 8;   // waves per bf16 prefill workgroup
 constexpr int kPrefillStages = 3;  // LDS ring depth of the bf16 prefill kernel
 
-template <int D>
+template <int CT, int D>
 hipError_t launch_prefill_mfma(const AttnArgs& a, const PrefillPlan& p, int n_tiles, hipStream_t stream) {
   constexpr size_t lds = 2 * kPrefillStages * 4 * kBlock * D * sizeof(uint16_t);
-  auto kern = prefill_mfma_kernel<D, kPrefillWaves, kPrefillStages>;
+  auto kern = prefill_mfma_kernel<CT, D, kPrefillWaves, kPrefillStages>;
   // The ring exceeds the default 64 KB of dynamic LDS; raise the limit once
   // per device (each GPU keeps its own function attributes).
   static std::atomic<unsigned long long> ready{0};
@@ -1201,7 +1268,7 @@ template <int DT, int D>
 struct PrefillL {
   static hipError_t run(const AttnArgs& a, const PrefillPlan& p, int n_tiles, hipStream_t stream) {
     if (n_tiles == 0) return hipSuccess;
-    if (DT == 0) return launch_prefill_mfma<D>(a, p, n_tiles, stream);
+    if constexpr (DT == 0 || DT == 2) return launch_prefill_mfma<DT, D>(a, p, n_tiles, stream);
     hipLaunchKernelGGL((prefill_kernel<DT, D>), dim3(n_tiles, a.hkv), dim3(64 * kWavesPerGroup), 0, stream, a, p);
     return hipGetLastError();
   }

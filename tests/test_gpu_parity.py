@@ -162,14 +162,15 @@ def few_key_specs(rng):
     return [specs[i] for i in order]
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
 @pytest.mark.parametrize("seed", [0, 1, 2, 3])
-def test_few_key_rows_at_rounding_floor(torch_gpu, seed):
+def test_few_key_rows_at_rounding_floor(torch_gpu, seed, dtype):
     """Rows that see few keys carry each output on a handful of
     probabilities, whose bf16 rounding does not average out: such rows must
     come out within 5e-4 of the exact result correctly rounded to bf16."""
     rng = np.random.default_rng(700 + seed)
-    b = make_batch(few_key_specs(rng), HeadSpec(32, 8, 128), "bf16", rng)
-    d, out, _ = check_batch(b, f"few-key rows seed {seed}")
+    b = make_batch(few_key_specs(rng), HeadSpec(32, 8, 128), dtype, rng)
+    d, out, _ = check_batch(b, f"few-key rows seed {seed} {dtype}")
     o_ref, _ = oracle_for(b)
     keys = np.concatenate([b.seq_lens[s] - b.q_lens[s] + 1 + np.arange(b.q_lens[s]) for s in range(b.num_seqs)])
     few = keys <= 48
@@ -217,17 +218,19 @@ def test_rope_append_then_attention(torch_gpu, dtype, heads, rope_dim):
     assert np.abs(lse.cpu().numpy().astype(np.float64)[rows] - l_ref[rows]).max() <= LSE_TOL[dtype]
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
 @pytest.mark.parametrize("heads", SPLIT_MIXES, ids=lambda h: f"hq{h[0]}_hkv{h[1]}_d{h[2]}")
-def test_prefill_kv_splits(torch_gpu, heads):
+def test_prefill_kv_splits(torch_gpu, heads, dtype):
     rng = np.random.default_rng(40 + heads[1])
-    b = make_batch(split_specs(rng), HeadSpec(*heads, 16), "bf16", rng)
+    b = make_batch(split_specs(rng), HeadSpec(*heads, 16), dtype, rng)
     sh = mpa.make_shape(num_seqs=b.num_seqs, num_q_heads=heads[0], num_kv_heads=heads[1], head_dim=heads[2],
                         num_blocks=b.num_blocks, max_blocks_per_seq=b.block_tables.shape[1],
-                        total_q_tokens=b.total_q, scale=b.scale, dtype=mpa.MPA_BF16)
+                        total_q_tokens=b.total_q, scale=b.scale,
+                        dtype=mpa.MPA_FP8 if dtype == "fp8" else mpa.MPA_BF16, k_scale=b.k_scale, v_scale=b.v_scale)
     info = mpa.plan_info(sh, b.seq_lens, b.query_start_loc)
-    say(f"[gpu] kv splits {heads}: up to {info.prefill_max_splits} splits, {info.num_prefill_tiles} workgroups")
+    say(f"[gpu] kv splits {heads} {dtype}: up to {info.prefill_max_splits} splits, {info.num_prefill_tiles} workgroups")
     assert info.prefill_max_splits > 1
-    check_batch(b, f"kv splits {heads}")
+    check_batch(b, f"kv splits {heads} {dtype}")
 
 
 def test_decode_only_and_prefill_only(torch_gpu):
