@@ -146,7 +146,9 @@ int mpa_kv_append(const mpa_shape* shape, const void* k_new, const void* v_new, 
  *   y[j + R/2] = x[j + R/2] * c + x[j] * s
  * and y[i] = x[i] for i >= R (partial rotary when R < d).  Each product and
  * each sum is rounded to float32 (no fused multiply-add), the result to the
- * cache's element type (bf16: nearest even).
+ * row's element type (bf16: nearest even).  With an fp8 cache the rotated
+ * key, so rounded to bf16, is then stored as a plain new key would be (the
+ * E4M3 code of y * (1 / k_scale)); q stays bf16.
  *
  * q                 device [T][Hq][d], rotated in place
  * rope_cos_sin      device float32 [rope_max_pos][R/2][2] (cos, sin), e.g.

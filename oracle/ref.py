@@ -34,7 +34,9 @@ The KV cache may also hold fp8 codes (OCP E4M3 with one scale per tensor,
 dtype "fp8"; queries, new rows and outputs stay bf16).  The paper is silent
 on cache precision; the reading is that a value x is stored as the E4M3
 code nearest to x / scale (ties to even, saturating at 448; ``fp8_codes``)
-and read back as code value * scale.
+and read back as code value * scale.  With both (rotation and an fp8
+cache), the rows are rotated as bf16 rows and the rotated key is then
+stored as any new key is: ``fp8_codes`` of the ``rope_reference`` result.
 
 Cache layout read here (the library header's definition), with
 ``X = 8`` elements (bf16, fp8) or 4 (f32): K element (block b, head h, slot t, dim i) is at

@@ -273,17 +273,20 @@ def kv_append(k_new, v_new, k_cache, v_cache, block_tables, seq_lens, query_star
 
 
 def kv_append_rope(q, k_new, v_new, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host,
-                   qsl_host, cos_sin, rope_dim=None, block_tables_host=None, stream=None) -> None:
+                   qsl_host, cos_sin, rope_dim=None, block_tables_host=None, stream=None, k_scale=1.0,
+                   v_scale=1.0) -> None:
     """mpa_kv_append_rope: q [T, Hq, d] rotated in place, k_new rotated into
     the cache, v_new appended; cos_sin is a float32 device tensor
-    [max_pos, R/2, 2] (rope_dim R defaults to 2 * cos_sin.shape[1])."""
+    [max_pos, R/2, 2] (rope_dim R defaults to 2 * cos_sin.shape[1]).  With
+    uint8 (fp8) caches the rows are stored as codes under the scales."""
     t, hkv, d = k_new.shape
     hq = q.shape[1]
     if rope_dim is None:
         rope_dim = 2 * int(cos_sin.shape[1])
     sl, qs = _host_i32(seq_lens_host), _host_i32(qsl_host)
     bth = None if block_tables_host is None else _host_i32(block_tables_host)
-    shape = make_shape(len(sl), hq, hkv, d, k_cache.shape[0], block_tables.shape[1], t, 1.0, _dtype_code(k_cache))
+    shape = make_shape(len(sl), hq, hkv, d, k_cache.shape[0], block_tables.shape[1], t, 1.0, _dtype_code(k_cache),
+                       k_scale=k_scale, v_scale=v_scale)
     rc = lib().mpa_kv_append_rope(
         ctypes.byref(shape), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(block_tables),
         _ptr(seq_lens), _ptr(query_start_loc), _i32p(sl), _i32p(qs), _i32p(bth), _ptr(cos_sin), int(rope_dim),

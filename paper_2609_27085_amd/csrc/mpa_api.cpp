@@ -399,7 +399,6 @@ int mpa_kv_append_rope(const mpa_shape* shape, void* q, const void* k_new, const
   if (!shape) return MPA_ERR_INVALID;
   if (rope_dim <= 0 || rope_dim % 16 != 0 || rope_dim > shape->head_dim || rope_max_pos <= 0)
     return MPA_ERR_INVALID;
-  if (shape->dtype == MPA_FP8) return MPA_ERR_UNSUPPORTED;  // the rotation is built for bf16 and f32 caches
   if (shape->total_q_tokens > 0 && (!q || !rope_cos_sin)) return MPA_ERR_INVALID;
   if (seq_lens_host && shape->num_seqs > 0)
     for (int s = 0; s < shape->num_seqs; ++s)

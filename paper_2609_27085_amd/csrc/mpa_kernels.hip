@@ -1022,6 +1022,24 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   if (a.lse && h == 0) a.lse[(size_t)(t0 + i) * a.hq + head] = (m_ref * c + log2f(lt)) * kLn2;
 }
 
+// Stores chunk c (8 consecutive bf16 elements, packed) of a new key row and
+// of a new value row into slot `slot` of cache head `head` of an fp8 cache:
+// each element x becomes the E4M3 code of x * (1 / scale).
+template <int D>
+__device__ inline void store_fp8_chunk(const AppendArgs& a, size_t head, int c, int slot, u32x4 kw, u32x4 vw) {
+  constexpr int NC = D / 8;
+  float kx[8], vx[8];
+  Tr<0>::unpack(kw, kx);
+  Tr<0>::unpack(vw, vx);
+  u32x2 kc = {0u, 0u};
+#pragma unroll
+  for (int e = 0; e < 8; ++e) kc[e / 4] |= f32_to_e4m3(kx[e] * a.inv_k_scale) << (8 * (e % 4));
+  *reinterpret_cast<u32x2*>(reinterpret_cast<uint8_t*>(a.k_cache) + ((head * NC + c) * kBlock + slot) * 8) = kc;
+  uint8_t* vc = reinterpret_cast<uint8_t*>(a.v_cache) + (head * D + c * 8) * kBlock + slot;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) vc[e * kBlock] = (uint8_t)f32_to_e4m3(vx[e] * a.inv_v_scale);
+}
+
 // ---------------------------------------------------------------------------
 // Append: one wave per new token.  The token's sequence comes from the
 // kernel-argument plan (directly when every sequence of the plan adds one
@@ -1055,17 +1073,8 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a, AppendPlan p)
     const uint16_t* vn = reinterpret_cast<const uint16_t*>(a.v_new) + (size_t)t * a.hkv * D;
     for (int ci = lane; ci < nchunk; ci += 64) {
       const int h = ci / NC, c = ci - h * NC;
-      const size_t head = (size_t)blk * a.hkv + h;
-      float kx[8], vx[8];
-      Tr<0>::unpack(*reinterpret_cast<const u32x4*>(kn + h * D + c * 8), kx);
-      Tr<0>::unpack(*reinterpret_cast<const u32x4*>(vn + h * D + c * 8), vx);
-      u32x2 kc = {0u, 0u};
-#pragma unroll
-      for (int e = 0; e < 8; ++e) kc[e / 4] |= f32_to_e4m3(kx[e] * a.inv_k_scale) << (8 * (e % 4));
-      *reinterpret_cast<u32x2*>(reinterpret_cast<uint8_t*>(a.k_cache) + ((head * NC + c) * kBlock + slot) * 8) = kc;
-      uint8_t* vc = reinterpret_cast<uint8_t*>(a.v_cache) + (head * D + c * 8) * kBlock + slot;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) vc[e * kBlock] = (uint8_t)f32_to_e4m3(vx[e] * a.inv_v_scale);
+      store_fp8_chunk<D>(a, (size_t)blk * a.hkv + h, c, slot, *reinterpret_cast<const u32x4*>(kn + h * D + c * 8),
+                         *reinterpret_cast<const u32x4*>(vn + h * D + c * 8));
     }
   } else {
   for (int c0 = 0; c0 < nchunk; c0 += 64 * U) {
@@ -1132,7 +1141,8 @@ __device__ inline u32x4 rope_chunk(const typename Tr<DT>::Elem* row, int c, int 
 // divides 64), so a pass loads every partner chunk before it stores any.
 template <int DT, int D>
 __global__ __launch_bounds__(256) void rope_append_kernel(AppendArgs a, AppendPlan p, RopeArgs r) {
-  using T = Tr<DT>;
+  constexpr int RT = DT == 2 ? 0 : DT;  // queries and new rows: bf16 beside an fp8 cache
+  using T = Tr<RT>;
   using E = typename T::Elem;
   constexpr int X = T::X;
   constexpr int NC = D / X;
@@ -1151,7 +1161,7 @@ __global__ __launch_bounds__(256) void rope_append_kernel(AppendArgs a, AppendPl
   for (int c0 = 0; c0 < r.hq * NC; c0 += 64) {
     const int ci = c0 + lane;
     if (ci >= r.hq * NC) break;
-    const u32x4 y = rope_chunk<DT>(q + (ci / NC) * D, ci % NC, r.half, cs);
+    const u32x4 y = rope_chunk<RT>(q + (ci / NC) * D, ci % NC, r.half, cs);
     *reinterpret_cast<u32x4*>(q + (ci / NC) * D + (ci % NC) * X) = y;
   }
 
@@ -1163,8 +1173,14 @@ __global__ __launch_bounds__(256) void rope_append_kernel(AppendArgs a, AppendPl
   for (int ci = lane; ci < a.hkv * NC; ci += 64) {
     const int h = ci / NC, c = ci - h * NC;
     const size_t head = (size_t)blk * a.hkv + h;
+    if constexpr (DT == 2) {
+      // fp8 cache: the rotated key, rounded to bf16, is quantized like a plain new key
+      store_fp8_chunk<D>(a, head, c, slot, rope_chunk<RT>(kn + h * D, c, r.half, cs),
+                         *reinterpret_cast<const u32x4*>(vn + h * D + c * X));
+      continue;
+    }
     *reinterpret_cast<u32x4*>(reinterpret_cast<E*>(a.k_cache) + ((head * NC + c) * kBlock + slot) * X) =
-        rope_chunk<DT>(kn + h * D, c, r.half, cs);
+        rope_chunk<RT>(kn + h * D, c, r.half, cs);
     E vv[X];
 #pragma unroll
     for (int e = 0; e < X; ++e) vv[e] = vn[h * D + c * X + e];
@@ -1199,15 +1215,11 @@ struct AppendL {
 template <int DT, int D>
 struct RopeAppendL {
   static hipError_t run(const AppendArgs& a, const AppendPlan& p, const RopeArgs& r, hipStream_t stream) {
-    if constexpr (DT == 2) {
-      return hipErrorInvalidValue;  // not built for fp8 caches (the host rejects it first)
-    } else {
-      const int tokens = p.tok_start[p.n_seqs];
-      if (tokens == 0) return hipSuccess;
-      hipLaunchKernelGGL((rope_append_kernel<DT, D>), dim3((tokens + kWavesPerGroup - 1) / kWavesPerGroup),
-                         dim3(64 * kWavesPerGroup), 0, stream, a, p, r);
-      return hipGetLastError();
-    }
+    const int tokens = p.tok_start[p.n_seqs];
+    if (tokens == 0) return hipSuccess;
+    hipLaunchKernelGGL((rope_append_kernel<DT, D>), dim3((tokens + kWavesPerGroup - 1) / kWavesPerGroup),
+                       dim3(64 * kWavesPerGroup), 0, stream, a, p, r);
+    return hipGetLastError();
   }
 };
 

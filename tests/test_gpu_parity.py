@@ -186,33 +186,38 @@ def rope_table(max_pos, rope_dim, base=10000.0):
     return np.stack([np.cos(ang), np.sin(ang)], axis=-1).astype(np.float32)
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dtype", ["bf16", "f32", "fp8"])
 @pytest.mark.parametrize("heads,rope_dim", [((32, 8, 128), 128), ((8, 2, 64), 32), ((16, 4, 128), 64)],
                          ids=["d128_full", "d64_r32", "d128_r64"])
 def test_rope_append_then_attention(torch_gpu, dtype, heads, rope_dim):
     """mpa_kv_append_rope: the rotated queries (in place) and the cache bit for
-    bit against the oracle's rotation, then attention on the rotated rows."""
+    bit against the oracle's rotation, then attention on the rotated rows.
+    With an fp8 cache the rows are bf16: the rotation is the bf16 one and the
+    rotated key is then stored as the append stores any new key."""
     torch = torch_gpu
     rng = np.random.default_rng(80 + rope_dim)
     b = make_batch(mixed_specs(rng), HeadSpec(*heads, 16), dtype, rng)
+    rd = "bf16" if dtype == "fp8" else dtype  # element type of q and the new rows
     say(f"[gpu] rope append: S={b.num_seqs} T={b.total_q} heads={heads} R={rope_dim} dtype={dtype}")
     table = rope_table(int(b.seq_lens.max()) + 7, rope_dim)
     d = to_device(b)
     mpa.kv_append_rope(d.q, d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
                        d.seq_lens_host, d.qsl_host, torch.from_numpy(table).cuda(),
-                       block_tables_host=d.block_tables_host)
+                       block_tables_host=d.block_tables_host, k_scale=d.k_scale, v_scale=d.v_scale)
     torch.cuda.synchronize()
     pos = ref.new_token_positions(b.seq_lens, b.query_start_loc)
-    q_rot = ref.rope_reference(b.q, pos, table, rope_dim, dtype)
-    k_rot = ref.rope_reference(b.k_new, pos, table, rope_dim, dtype)
-    assert tensor_to_raw(d.q, dtype).tobytes() == np.ascontiguousarray(q_rot).tobytes(), "rotated q not bit-exact"
+    q_rot = ref.rope_reference(b.q, pos, table, rope_dim, rd)
+    k_rot = ref.rope_reference(b.k_new, pos, table, rope_dim, rd)
+    assert tensor_to_raw(d.q, rd).tobytes() == np.ascontiguousarray(q_rot).tobytes(), "rotated q not bit-exact"
     kc, vc = ref.append_reference(b.k_cache, b.v_cache, k_rot, b.v_new, b.block_tables, b.seq_lens,
-                                  b.query_start_loc, b.heads.block_size, dtype)
+                                  b.query_start_loc, b.heads.block_size, dtype, k_scale=b.k_scale,
+                                  v_scale=b.v_scale)
     assert tensor_to_raw(d.k_cache, dtype).tobytes() == kc.tobytes(), "rotated K append not bit-exact"
     assert tensor_to_raw(d.v_cache, dtype).tobytes() == vc.tobytes(), "V append not bit-exact"
     out, lse = run_step(d, append=False)
     o_ref, l_ref = ref.attention_reference(q_rot, b.k_cache, b.v_cache, k_rot, b.v_new, b.block_tables, b.seq_lens,
-                                           b.query_start_loc, b.scale, heads[1], 16, dtype)
+                                           b.query_start_loc, b.scale, heads[1], 16, dtype, k_scale=b.k_scale,
+                                           v_scale=b.v_scale)
     rows = np.repeat(b.q_lens > 0, b.q_lens)
     assert_close(as_f64(out)[rows], o_ref[rows], dtype, "rope attention")
     assert np.abs(lse.cpu().numpy().astype(np.float64)[rows] - l_ref[rows]).max() <= LSE_TOL[dtype]
