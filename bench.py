@@ -328,7 +328,7 @@ def main(argv=None) -> int:
         kernel = "decode_kernel+merge_kernel"
     else:
         achieved, peak, unit, bound = pre_tflops, MFMA_BF16_PEAK_TFLOPS, "TFLOP/s", "mfma"
-        kernel = "prefill_mfma_kernel" if args.kv == "bf16" else "prefill_kernel"
+        kernel = "prefill_mfma_kernel"
     roofline = {
         "bound": bound,
         "achieved": round(achieved, 2),
