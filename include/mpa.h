@@ -241,7 +241,9 @@ const char* mpa_status_string(int status);
 typedef struct {
   int32_t num_decode_seqs;   /* sequences with q_len == 1 */
   int32_t num_prefill_seqs;  /* sequences with q_len > 1 */
-  int32_t split_tokens;      /* KV tokens per decode split */
+  int32_t split_tokens;      /* nominal KV tokens per decode split: a row of L keys is cut into
+                                ceil(L / split_tokens) parts of equal size, rounded up to whole
+                                blocks (the last part ends at L) */
   int32_t num_decode_items;  /* (sequence, split) work items */
   int32_t num_prefill_tiles; /* (sequence, query tile, KV split, KV head) work items */
   int32_t decode_launches;   /* decode kernel launches (sequence chunks) */

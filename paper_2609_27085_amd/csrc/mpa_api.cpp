@@ -75,6 +75,24 @@ int check_batch(const mpa_shape* sh, const int32_t* seq_lens, const int32_t* qsl
   return MPA_OK;
 }
 
+// How a decode row of L keys is split at nominal split size S: into
+// n = ceil(L / S) parts of equal size, rounded up to whole cache blocks, so
+// that the waves of a launch stream about the same number of bytes (a fixed
+// size S with a short remainder would leave the short waves idle while the
+// full ones finish).  The last part ends at L; `parts` can be below n when
+// the rounding makes the earlier parts cover L sooner.
+struct RowSplit {
+  int parts;
+  int tokens;  // keys per part, a multiple of the block size
+};
+
+RowSplit row_split(int L, int S) {
+  const int n = std::max(1, (L + S - 1) / S);
+  const int per = (L + n - 1) / n;
+  const int tokens = std::max(kBlock, (per + kBlock - 1) / kBlock * kBlock);
+  return {std::max(1, (L + tokens - 1) / tokens), tokens};
+}
+
 // KV tokens per decode split.  Every (split, KV head) is one wave, and a
 // wave's time is about proportional to its tokens plus a fixed start-up cost,
 // so the step takes about ceil(waves / slots) * (split + overhead), where
@@ -95,7 +113,7 @@ int choose_split(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens) {
   int best = 1024;
   for (int split = 128; split <= 1024; split += kBlock) {
     long items = 0;
-    for (int s : b.decode) items += std::max(1, (seq_lens[s] + split - 1) / split);
+    for (int s : b.decode) items += row_split(seq_lens[s], split).parts;
     const long waves = items * sh->num_kv_heads;
     const long cost = ((waves + slots - 1) / slots) * (split + overhead);
     if (best_cost < 0 || cost < best_cost) {
@@ -109,7 +127,7 @@ int choose_split(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens) {
 long decode_items(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens, int split) {
   (void)sh;
   long n = 0;
-  for (int s : b.decode) n += std::max(1, (seq_lens[s] + split - 1) / split);
+  for (int s : b.decode) n += row_split(seq_lens[s], split).parts;
   return n;
 }
 
@@ -320,8 +338,8 @@ int mpa_predict_step(const mpa_shape* shape, const int32_t* seq_lens_host, const
     for (size_t k = c0; k < c1; ++k) {
       const int L = seq_lens_host[b.decode[k]];
       bytes += (double)L * head_bytes * shape->num_kv_heads;
-      wave = std::max(wave, (double)std::min(L, split) * head_bytes);
-      split_any |= L > split;
+      wave = std::max(wave, (double)std::min(L, row_split(L, split).tokens) * head_bytes);
+      split_any |= row_split(L, split).parts > 1;
     }
     t.decode_us += r.decode_fixed_us + std::max(bytes / (r.decode_gbs * 1e3), wave / (r.decode_wave_gbs * 1e3));
     if (split_any) t.decode_us += r.merge_us;
@@ -376,7 +394,7 @@ size_t mpa_workspace_size(const mpa_shape* shape, const int32_t* seq_lens_host, 
   if (check_batch(shape, seq_lens_host, qsl_host, nullptr, false, &b) != MPA_OK) return 0;
   const int split = choose_split(shape, b, seq_lens_host);
   bool any_split = false;
-  for (int s : b.decode) any_split |= seq_lens_host[s] > split;
+  for (int s : b.decode) any_split |= row_split(seq_lens_host[s], split).parts > 1;
   const long ditems = decode_items(shape, b, seq_lens_host, split);
   const long pitems = prefill_items(prefill_splits(shape, b, seq_lens_host, qsl_host, ditems), b, qsl_host);
   if (!any_split && pitems == 0) return 0;
@@ -443,7 +461,7 @@ int run_attention(int phases, const mpa_shape* shape, const void* q, const void*
       prefill_splits(shape, all, seq_lens_host, query_start_loc_host, ditems);
   const long items = ditems + prefill_items(psplit, all, query_start_loc_host);
   bool any_split = false;
-  for (int s : b.decode) any_split |= seq_lens_host[s] > split;
+  for (int s : b.decode) any_split |= row_split(seq_lens_host[s], split).parts > 1;
   if (!b.prefill.empty())
     for (const auto& ps : psplit) any_split |= ps.nsplit > 1;
   if (any_split) {
@@ -482,14 +500,15 @@ int run_attention(int phases, const mpa_shape* shape, const void* q, const void*
       memset(&p, 0, sizeof(p));
       const size_t c1 = std::min(b.decode.size(), c0 + mpa::kMaxPlanSeqs);
       p.n_seqs = (int32_t)(c1 - c0);
-      p.split_tokens = split;
       p.item_base = (int32_t)base;
       int acc = 0;
       for (size_t k = c0; k < c1; ++k) {
         const int s = b.decode[k];
+        const RowSplit rs = row_split(seq_lens_host[s], split);
         p.seq[k - c0] = s;
+        p.split_tokens[k - c0] = rs.tokens;
         p.item_start[k - c0] = acc;
-        acc += std::max(1, (seq_lens_host[s] + split - 1) / split);
+        acc += rs.parts;
       }
       p.item_start[c1 - c0] = acc;
       base += acc;

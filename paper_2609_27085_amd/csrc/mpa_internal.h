@@ -36,14 +36,16 @@ struct AttnArgs {
 };
 
 // Decode work for up to kMaxPlanSeqs sequences: item k of this launch is
-// split (k - item_start[j]) of sequence seq[j], where item_start[j] <= k <
-// item_start[j+1].  Its partial results live at workspace slot
+// split x = k - item_start[j] of sequence seq[j], where item_start[j] <= k <
+// item_start[j+1]; it covers keys [x * split_tokens[j], (x + 1) *
+// split_tokens[j]) (a multiple of the block size; the last split ends at the
+// sequence's length).  Its partial results live at workspace slot
 // item_base + k.
 struct DecodePlan {
   int32_t n_seqs;
-  int32_t split_tokens;
   int32_t item_base;
   int32_t seq[kMaxPlanSeqs];
+  int32_t split_tokens[kMaxPlanSeqs];
   int32_t item_start[kMaxPlanSeqs + 1];
 };
 

@@ -444,8 +444,8 @@ __global__ __launch_bounds__(256) void decode_kernel(AttnArgs a, DecodePlan p) {
   const int split = item - p.item_start[j];
   const int nsplit = p.item_start[j + 1] - p.item_start[j];
   const int L = a.seq_lens[s];
-  const int k0 = split * p.split_tokens;
-  const int k1 = min(L, k0 + p.split_tokens);
+  const int k0 = split * p.split_tokens[j];
+  const int k1 = min(L, k0 + p.split_tokens[j]);
   const int trow = a.qsl[s];
   const int G = a.hq / a.hkv;
   const int n = lane & 15, grp = lane >> 4;

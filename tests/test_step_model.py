@@ -130,3 +130,19 @@ def test_shape_dependence(L):
     a = predict([8192] * 32).decode_us
     b = predict([2048] * 128).decode_us
     assert abs(a - b) / a < 0.05
+
+
+def test_decode_rows_split_into_equal_block_aligned_parts(L):
+    """A long decode row is cut into ceil(L / S) parts of equal size rounded up
+    to whole blocks, not S-sized parts plus a short remainder: the model's
+    largest wave (one part of one KV head) shows the part size."""
+    sl, qsl = batch([9000])
+    info = mpa.plan_info(shape(sl, qsl), sl, qsl)
+    S = info.split_tokens
+    n = -(-9000 // S)
+    part = -(-(-(-9000 // n)) // 16) * 16
+    assert info.num_decode_items == -(-9000 // part) == n
+    assert part <= S and (n - 1) * part < 9000 <= n * part
+    r = unit_rates(decode_gbs=1e12, decode_wave_gbs=1.0)
+    t = predict([9000], rates=r)
+    assert math.isclose(t.decode_us, part * 2 * 128 * 2 / 1e3, rel_tol=1e-12)
