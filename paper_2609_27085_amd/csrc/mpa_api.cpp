@@ -220,9 +220,35 @@ int run_append(const mpa_shape* shape, const void* k_new, const void* v_new, voi
   a.inv_v_scale = shape->dtype == MPA_FP8 ? 1.f / shape->v_scale : 1.f;
   (void)seq_lens;
   (void)query_start_loc;
+  // single-token sequences one wave per token; with the rotary embedding
+  // (which also rotates q, token by token) every sequence
   std::vector<int> seqs(b.decode);
-  seqs.insert(seqs.end(), b.prefill.begin(), b.prefill.end());
+  if (rope) seqs.insert(seqs.end(), b.prefill.begin(), b.prefill.end());
   clear_stale_hip_error();
+  // multi-token sequences one wave per (cache block, KV head)
+  if (!rope) {
+    for (size_t c0 = 0; c0 < b.prefill.size(); c0 += mpa::kMaxPrefillSeqs) {
+      mpa::AppendBlockPlan p;
+      memset(&p, 0, sizeof(p));
+      const size_t c1 = std::min(b.prefill.size(), c0 + mpa::kMaxPrefillSeqs);
+      p.n_seqs = (int32_t)(c1 - c0);
+      int acc = 0;
+      for (size_t k = c0; k < c1; ++k) {
+        const int s = b.prefill[k];
+        const int ql = query_start_loc_host[s + 1] - query_start_loc_host[s];
+        const int pos0 = seq_lens_host[s] - ql;
+        p.seq[k - c0] = s;
+        p.row0[k - c0] = query_start_loc_host[s];
+        p.pos0[k - c0] = pos0;
+        p.ntok[k - c0] = ql;
+        p.unit_start[k - c0] = acc;
+        acc += (pos0 + ql - 1) / kBlock - pos0 / kBlock + 1;
+      }
+      p.unit_start[c1 - c0] = acc;
+      if (mpa::launch_append_blocks(a, p, shape->dtype, shape->head_dim, (hipStream_t)stream) != hipSuccess)
+        return MPA_ERR_HIP;
+    }
+  }
   for (size_t c0 = 0; c0 < seqs.size(); c0 += mpa::kMaxPlanSeqs) {
     mpa::AppendPlan p;
     memset(&p, 0, sizeof(p));

@@ -101,9 +101,26 @@ struct AppendPlan {
   int32_t tok_start[kMaxPlanSeqs + 1];
 };
 
+// Append work for up to kMaxPrefillSeqs sequences that add several tokens,
+// by cache block: unit u of this launch is the
+// (u - unit_start[j])-th cache block touched by the new tokens of sequence
+// seq[j].  Those tokens are query rows row0[j] .. row0[j] + ntok[j] - 1 at
+// positions pos0[j] .. pos0[j] + ntok[j] - 1.
+struct AppendBlockPlan {
+  int32_t n_seqs;
+  int32_t seq[kMaxPrefillSeqs];
+  int32_t row0[kMaxPrefillSeqs];
+  int32_t pos0[kMaxPrefillSeqs];
+  int32_t ntok[kMaxPrefillSeqs];
+  int32_t unit_start[kMaxPrefillSeqs + 1];
+};
+
 // Launchers (mpa_kernels.hip).  dtype: 0 = bf16, 1 = f32, 2 = fp8 cache.  Return the HIP
 // error of the launch.
 hipError_t launch_append(const AppendArgs& a, const AppendPlan& p, int dtype, int head_dim, hipStream_t stream);
+// The same bits for multi-token sequences, one wave per (cache block, KV head).
+hipError_t launch_append_blocks(const AppendArgs& a, const AppendBlockPlan& p, int dtype, int head_dim,
+                                hipStream_t stream);
 hipError_t launch_rope_append(const AppendArgs& a, const AppendPlan& p, const RopeArgs& r, int dtype, int head_dim,
                               hipStream_t stream);
 // Decode waves the current device holds at once (2048 without a device).

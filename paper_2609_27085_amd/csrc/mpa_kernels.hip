@@ -1104,6 +1104,103 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a, AppendPlan p)
   }
 }
 
+// Append for sequences that add several tokens: one wave per (cache block,
+// KV head) writes every new token of the block.  K pieces (chunk c, slot t)
+// are taken slot-fastest, so the stores of a chunk row are one contiguous
+// run; each lane gathers D / 64 dims of every token, so that a block's V^T
+// row of a dim (16 slots) is stored at once when the block is written whole
+// (element by element for the slots of a partly written block).  The bits
+// stored are the plain append's.
+template <int DT, int D>
+__global__ __launch_bounds__(256) void append_block_kernel(AppendArgs a, AppendBlockPlan p) {
+  constexpr int RT = DT == 2 ? 0 : DT;  // new rows: bf16 beside an fp8 cache
+  using NE = typename Tr<RT>::Elem;
+  using CE = typename Tr<DT>::Elem;
+  constexpr int X = Tr<DT>::X;           // elements per K chunk of the cache
+  constexpr int NC = D / X;
+  constexpr int DPL = D / 64;            // V dims per lane
+  static_assert((NC * kBlock) % 64 == 0, "K pieces fill whole passes of the wave");
+  const int lane = threadIdx.x & 63;
+  const int w = blockIdx.x * kWavesPerGroup + wave_uniform(threadIdx.x >> 6);
+  const int unit = w / a.hkv, h = w - unit * a.hkv;
+  if (unit >= p.unit_start[p.n_seqs]) return;
+  const int j = upper_index(p.unit_start, p.n_seqs, unit);
+  const int first = p.pos0[j], end = p.pos0[j] + p.ntok[j];  // new positions [first, end)
+  const int b = first / kBlock + (unit - p.unit_start[j]);   // cache block index in the sequence
+  const int s0 = max(first, b * kBlock) - b * kBlock;          // its new slots [s0, s1)
+  const int s1 = min(end, b * kBlock + kBlock) - b * kBlock;
+  const int blk = a.block_tables[(size_t)p.seq[j] * a.mb + b];
+  if (blk < 0 || blk >= a.nb) return;
+  const size_t head = (size_t)blk * a.hkv + h;
+  const size_t rstride = (size_t)a.hkv * D;                    // elements between token rows
+  const int row_s0 = p.row0[j] + b * kBlock + s0 - first;      // query row of slot s0
+  const NE* kn = reinterpret_cast<const NE*>(a.k_new) + (size_t)h * D;
+  const NE* vn = reinterpret_cast<const NE*>(a.v_new) + (size_t)h * D;
+
+  // K: piece (chunk c, slot t) of the block from token row row_s0 + t - s0;
+  // all of a lane's loads are issued before its stores
+  constexpr int KP = NC * kBlock / 64;  // pieces per lane
+  u32x4 kw[KP];
+#pragma unroll
+  for (int u = 0; u < KP; ++u) {
+    const int pc = 64 * u + lane, c = pc / kBlock, t = pc % kBlock;
+    const int row = row_s0 + min(max(t, s0), s1 - 1) - s0;  // slots outside [s0, s1) reload a valid row
+    kw[u] = *reinterpret_cast<const u32x4*>(kn + (size_t)row * rstride + c * X);
+  }
+#pragma unroll
+  for (int u = 0; u < KP; ++u) {
+    const int pc = 64 * u + lane, c = pc / kBlock, t = pc % kBlock;
+    if (t < s0 || t >= s1) continue;
+    CE* dst = reinterpret_cast<CE*>(a.k_cache) + ((head * NC + c) * kBlock + t) * X;
+    if constexpr (DT == 2) {
+      float kx[8];
+      Tr<0>::unpack(kw[u], kx);
+      u32x2 kc = {0u, 0u};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) kc[e / 4] |= f32_to_e4m3(kx[e] * a.inv_k_scale) << (8 * (e % 4));
+      *reinterpret_cast<u32x2*>(dst) = kc;
+    } else {
+      *reinterpret_cast<u32x4*>(dst) = kw[u];
+    }
+  }
+
+  // V: this lane's dims d = DPL * lane + i of every new token of the block
+  CE vals[kBlock][DPL];
+#pragma unroll
+  for (int t = 0; t < kBlock; ++t) {
+    if (t < s0 || t >= s1) continue;
+    const NE* src = vn + (size_t)(row_s0 + t - s0) * rstride + DPL * lane;
+#pragma unroll
+    for (int i = 0; i < DPL; ++i) {
+      if constexpr (DT == 2) {
+        vals[t][i] = (uint8_t)f32_to_e4m3(__uint_as_float((unsigned)src[i] << 16) * a.inv_v_scale);
+      } else {
+        vals[t][i] = src[i];
+      }
+    }
+  }
+  CE* vdst = reinterpret_cast<CE*>(a.v_cache) + (head * D + DPL * lane) * kBlock;
+  if (s0 == 0 && s1 == kBlock) {
+#pragma unroll
+    for (int i = 0; i < DPL; ++i) {
+      constexpr int PER = 16 / sizeof(CE);  // elements per 16-byte store
+#pragma unroll
+      for (int q = 0; q < kBlock / PER; ++q) {
+        CE piece[PER];
+#pragma unroll
+        for (int e = 0; e < PER; ++e) piece[e] = vals[q * PER + e][i];
+        *reinterpret_cast<u32x4*>(vdst + i * kBlock + q * PER) = __builtin_bit_cast(u32x4, piece);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int t = 0; t < kBlock; ++t)
+      if (t >= s0 && t < s1)
+#pragma unroll
+        for (int i = 0; i < DPL; ++i) vdst[i * kBlock + t] = vals[t][i];
+  }
+}
+
 // Rotary embedding of 16-byte chunk c of one head row (rotate-half form):
 // element i < half pairs with i + half; with the position's angle row cs
 // (cos, sin interleaved per pair), y_i = x_i cos - x_{i+half} sin and
@@ -1213,6 +1310,17 @@ struct AppendL {
 };
 
 template <int DT, int D>
+struct AppendBlockL {
+  static hipError_t run(const AppendArgs& a, const AppendBlockPlan& p, hipStream_t stream) {
+    const long waves = (long)p.unit_start[p.n_seqs] * a.hkv;
+    if (waves == 0) return hipSuccess;
+    hipLaunchKernelGGL((append_block_kernel<DT, D>), dim3((unsigned)((waves + kWavesPerGroup - 1) / kWavesPerGroup)),
+                       dim3(64 * kWavesPerGroup), 0, stream, a, p);
+    return hipGetLastError();
+  }
+};
+
+template <int DT, int D>
 struct RopeAppendL {
   static hipError_t run(const AppendArgs& a, const AppendPlan& p, const RopeArgs& r, hipStream_t stream) {
     const int tokens = p.tok_start[p.n_seqs];
@@ -1290,6 +1398,11 @@ struct PrefillL {
 
 hipError_t launch_append(const AppendArgs& a, const AppendPlan& p, int dtype, int head_dim, hipStream_t stream) {
   return dispatch<AppendL>(dtype, head_dim, a, p, stream);
+}
+
+hipError_t launch_append_blocks(const AppendArgs& a, const AppendBlockPlan& p, int dtype, int head_dim,
+                                hipStream_t stream) {
+  return dispatch<AppendBlockL>(dtype, head_dim, a, p, stream);
 }
 
 hipError_t launch_rope_append(const AppendArgs& a, const AppendPlan& p, const RopeArgs& r, int dtype, int head_dim,
