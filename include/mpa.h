@@ -267,7 +267,10 @@ int mpa_get_plan_info(const mpa_shape* shape, const int32_t* seq_lens_host,
  * own plan for the batch (decode splits, prefill query tiles, KV splits,
  * launches) and a few measured rates:
  *
- *   append  = append_fixed_us + (bytes read and written) / append_gbs
+ *   append  = per launch for single-token sequences: append_fixed_us +
+ *             (bytes read and written) / append_gbs; per launch for
+ *             multi-token sequences: max(append_block_us, bytes /
+ *             append_block_gbs)
  *   decode  = per launch: decode_fixed_us + max(KV bytes / decode_gbs,
  *             largest wave's KV bytes / decode_wave_gbs), plus merge_us per
  *             launch when a row is split
@@ -293,6 +296,8 @@ typedef struct {
   double prefill_merge_us;
   double prefill_fixup_us;
   int32_t prefill_slots;
+  double append_block_us;
+  double append_block_gbs;
 } mpa_rates;
 
 typedef struct {

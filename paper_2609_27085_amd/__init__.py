@@ -99,6 +99,8 @@ class MpaRates(ctypes.Structure):
         ("prefill_merge_us", ctypes.c_double),
         ("prefill_fixup_us", ctypes.c_double),
         ("prefill_slots", ctypes.c_int32),
+        ("append_block_us", ctypes.c_double),
+        ("append_block_gbs", ctypes.c_double),
     ]
 
 

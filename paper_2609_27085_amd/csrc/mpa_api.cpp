@@ -320,9 +320,14 @@ void mpa_default_rates(mpa_rates* r) {
   // Least-squares fit (log error) to the phase times bench.py measured on
   // one MI355X for decode8b, lent, agentic, budget0/256/1024/4096 and
   // longctx (seed 0, each phase less the ~5 us of its event record); the
-  // merge, few-key and wave figures are single kernel times from rocprofv3
-  r->append_fixed_us = 6.5;
-  r->append_gbs = 1140.0;
+  // merge, few-key and wave figures are single kernel times from rocprofv3.
+  // The append figures are fitted to the append phases alone: the
+  // per-token launch from decode8b and budget0, the per-block launch (a
+  // latency floor, then about 3.7 TB/s) from lent, budget4096 and longctx.
+  r->append_fixed_us = 3.9;
+  r->append_gbs = 545.0;
+  r->append_block_us = 17.0;
+  r->append_block_gbs = 3700.0;
   r->decode_fixed_us = 2.0;
   r->decode_gbs = 5600.0;
   r->decode_wave_gbs = 4.8;
@@ -344,15 +349,25 @@ int mpa_predict_step(const mpa_shape* shape, const int32_t* seq_lens_host, const
   mpa_rates def;
   mpa_default_rates(&def);
   const mpa_rates& r = rates ? *rates : def;
-  if (!(r.append_gbs > 0) || !(r.decode_gbs > 0) || !(r.decode_wave_gbs > 0) || r.prefill_slots <= 0)
+  if (!(r.append_gbs > 0) || !(r.append_block_gbs > 0) || !(r.decode_gbs > 0) || !(r.decode_wave_gbs > 0) ||
+      r.prefill_slots <= 0)
     return MPA_ERR_INVALID;
   const double elem = 2.0;  // bf16
   const double row_bytes = (double)shape->num_kv_heads * shape->head_dim * elem;  // one token's K (or V)
   mpa_step_time t = {0.0, 0.0, 0.0, 0.0};
 
-  // append: every new token's K and V read once and written once
-  if (shape->total_q_tokens > 0)
-    t.append_us = r.append_fixed_us + 4.0 * row_bytes * shape->total_q_tokens / (r.append_gbs * 1e3);
+  // append, launch by launch as run_append issues them: every new token's K
+  // and V read once and written once
+  for (size_t c0 = 0; c0 < b.decode.size(); c0 += mpa::kMaxPlanSeqs) {
+    const double tokens = (double)(std::min(b.decode.size(), c0 + mpa::kMaxPlanSeqs) - c0);
+    t.append_us += r.append_fixed_us + 4.0 * row_bytes * tokens / (r.append_gbs * 1e3);
+  }
+  for (size_t c0 = 0; c0 < b.prefill.size(); c0 += mpa::kMaxPrefillSeqs) {
+    double tokens = 0.0;
+    for (size_t k = c0; k < std::min(b.prefill.size(), c0 + mpa::kMaxPrefillSeqs); ++k)
+      tokens += qsl_host[b.prefill[k] + 1] - qsl_host[b.prefill[k]];
+    t.append_us += std::max(r.append_block_us, 4.0 * row_bytes * tokens / (r.append_block_gbs * 1e3));
+  }
 
   // decode, launch by launch as run_attention issues them
   const int split = choose_split(shape, b, seq_lens_host);

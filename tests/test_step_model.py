@@ -44,7 +44,8 @@ def unit_rates(**over):
     for k in ("append_fixed_us", "decode_fixed_us", "merge_us", "prefill_wg_us", "prefill_merge_us",
               "prefill_fixup_us"):
         setattr(r, k, 0.0)
-    r.append_gbs = r.decode_gbs = r.decode_wave_gbs = 1e12  # bandwidth terms ~0
+    r.append_block_us = 0.0
+    r.append_gbs = r.append_block_gbs = r.decode_gbs = r.decode_wave_gbs = 1e12  # bandwidth terms ~0
     r.prefill_tile_us = 1.0
     for k, v in over.items():
         setattr(r, k, v)
@@ -55,7 +56,7 @@ def test_default_rates_are_sane(L):
     r = mpa.default_rates()
     assert 1000 < r.decode_gbs <= 8000  # below the 8 TB/s datasheet peak
     assert r.prefill_slots == 256
-    assert r.prefill_tile_us > 0 and r.append_gbs > 0 and r.decode_wave_gbs > 0
+    assert r.prefill_tile_us > 0 and r.append_gbs > 0 and r.decode_wave_gbs > 0 and r.append_block_gbs > 0
 
 
 def test_step_is_sum_of_phases(L):
@@ -80,6 +81,13 @@ def test_append_and_decode_bandwidth_terms(L):
     r = unit_rates(append_gbs=1.0)
     t = predict([50, 60, 70], rates=r)
     assert math.isclose(t.append_us, 4 * 3 * 8 * 128 * 2 / 1e3, rel_tol=1e-12)
+    # multi-token sequences: their own launch, bytes over append_block_gbs,
+    # but never under append_block_us; single-token rows keep their launch
+    r = unit_rates(append_block_gbs=1.0)
+    t = predict(chunks=[(64, 128), (36, 0)], rates=r)
+    assert math.isclose(t.append_us, 4 * 100 * 8 * 128 * 2 / 1e3, rel_tol=1e-12)
+    r = unit_rates(append_block_us=1e6, append_fixed_us=7.0)
+    assert predict([50], [(64, 128)], rates=r).append_us == pytest.approx(1e6 + 7.0)
     # decode: K+V bytes of every context token, or the largest wave alone
     r = unit_rates(decode_gbs=2.0, decode_wave_gbs=1e12)
     t = predict([100, 300], rates=r)
