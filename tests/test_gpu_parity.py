@@ -238,6 +238,40 @@ def test_prefill_kv_splits(torch_gpu, heads, dtype):
     check_batch(b, f"kv splits {heads} {dtype}")
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_decode_split_boundaries(torch_gpu, dtype, monkeypatch):
+    """Decode rows whose lengths sit at and around multiples of a forced
+    128-token nominal split: every row is cut into ceil(L / 128) equal parts
+    rounded up to whole blocks, so part edges fall inside blocks of the
+    nominal grid and the last part is short or full."""
+    monkeypatch.setenv("MPA_SPLIT_TOKENS", "128")
+    lens = [1, 15, 16, 17, 127, 128, 129, 143, 144, 255, 256, 257, 383, 1000, 1025, 4097]
+    b = make_batch([SeqSpec(L, 1) for L in lens], HeadSpec(16, 4, 128), dtype, np.random.default_rng(70))
+    sh = mpa.make_shape(num_seqs=b.num_seqs, num_q_heads=16, num_kv_heads=4, head_dim=128, num_blocks=b.num_blocks,
+                        max_blocks_per_seq=b.block_tables.shape[1], total_q_tokens=b.total_q, scale=b.scale,
+                        dtype=mpa.MPA_FP8 if dtype == "fp8" else mpa.MPA_BF16, k_scale=b.k_scale, v_scale=b.v_scale)
+    info = mpa.plan_info(sh, b.seq_lens, b.query_start_loc)
+    assert info.split_tokens == 128
+    assert info.num_decode_items == sum(-(-L // 128) for L in lens)
+    check_batch(b, f"decode split boundaries {dtype}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32", "fp8"])
+def test_append_block_boundaries(torch_gpu, dtype):
+    """Multi-token appends (written by cache block) starting at every slot
+    alignment that matters and ending inside, at the start of and at the end
+    of a block, beside single-token appends: the whole pool bit for bit."""
+    specs = []
+    for p in (0, 1, 8, 15, 16, 17, 31):
+        for c in (2, 15, 16, 17, 33):
+            specs.append(SeqSpec(p + c, c))
+    specs += [SeqSpec(40, 1), SeqSpec(16, 1)]
+    rng = np.random.default_rng(71)
+    order = rng.permutation(len(specs))
+    b = make_batch([specs[i] for i in order], HeadSpec(8, 2, 64 if dtype == "f32" else 128), dtype, rng)
+    check_batch(b, f"append block boundaries {dtype}")
+
+
 def test_decode_only_and_prefill_only(torch_gpu):
     rng = np.random.default_rng(21)
     dec = [SeqSpec(int(c), 1) for c in rng.integers(1, 4000, size=20)]
