@@ -125,6 +125,11 @@ typedef struct {
  * seq_lens_host, query_start_loc_host            host copies (must match)
  * block_tables_host host copy [S][max_blocks_per_seq] or NULL; when given,
  *                   every block id the step uses is checked on the host.
+ * With MPA_DEBUG=1 in the environment (read at each call) the host also
+ * checks that the slots written are pairwise distinct and that none holds a
+ * key a sequence of the step reads (prefix blocks shared between sequences
+ * are read-only); this needs block_tables_host and visits every key of the
+ * step.  A violation, or a missing block_tables_host, gives MPA_ERR_INVALID.
  * Returns MPA_OK, or an error code with nothing launched.
  */
 int mpa_kv_append(const mpa_shape* shape, const void* k_new, const void* v_new, void* k_cache,

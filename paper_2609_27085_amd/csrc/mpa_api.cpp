@@ -10,6 +10,7 @@
 #include <algorithm>
 #include <functional>
 #include <queue>
+#include <unordered_set>
 #include <vector>
 
 #include "mpa.h"
@@ -195,6 +196,36 @@ long prefill_items(const std::vector<PrefillSplit>& sp, const Batch& b, const in
   return n;
 }
 
+// MPA_DEBUG=1 (read per call): before an append, the cache slots it writes
+// must be pairwise distinct, and none may hold a key that a sequence of the
+// step reads (prefix blocks shared between sequences are read-only).  Needs
+// the host copy of the block tables; without it the check cannot run and
+// the call is rejected.  Costs a pass over every key of the step.
+bool debug_checks() {
+  const char* e = getenv("MPA_DEBUG");
+  return e && e[0] == '1' && e[1] == '\0';
+}
+
+int check_append_slots(const mpa_shape* sh, const int32_t* seq_lens, const int32_t* qsl, const int32_t* bt) {
+  if (!bt) return MPA_ERR_INVALID;
+  std::unordered_set<int64_t> written;
+  auto slot_of = [&](int s, int p) {
+    return (int64_t)bt[(size_t)s * sh->max_blocks_per_seq + p / kBlock] * kBlock + p % kBlock;
+  };
+  for (int s = 0; s < sh->num_seqs; ++s) {
+    const int ql = qsl[s + 1] - qsl[s];
+    for (int p = seq_lens[s] - ql; p < seq_lens[s]; ++p)
+      if (!written.insert(slot_of(s, p)).second) return MPA_ERR_INVALID;  // two tokens, one slot
+  }
+  for (int s = 0; s < sh->num_seqs; ++s) {
+    const int ql = qsl[s + 1] - qsl[s];
+    if (ql == 0) continue;
+    for (int p = 0; p < seq_lens[s] - ql; ++p)
+      if (written.count(slot_of(s, p))) return MPA_ERR_INVALID;  // overwrites a key that is read
+  }
+  return MPA_OK;
+}
+
 // The append launches (plain, or with the rotary embedding when rope is
 // given): one wave per new token, up to kMaxPlanSeqs sequences per launch.
 int run_append(const mpa_shape* shape, const void* k_new, const void* v_new, void* k_cache, void* v_cache,
@@ -205,6 +236,10 @@ int run_append(const mpa_shape* shape, const void* k_new, const void* v_new, voi
   int rc = check_batch(shape, seq_lens_host, query_start_loc_host, block_tables_host, true, &b);
   if (rc != MPA_OK) return rc;
   if (shape->total_q_tokens == 0) return MPA_OK;
+  if (debug_checks()) {
+    rc = check_append_slots(shape, seq_lens_host, query_start_loc_host, block_tables_host);
+    if (rc != MPA_OK) return rc;
+  }
   if (!k_new || !v_new || !k_cache || !v_cache || !block_tables || !seq_lens || !query_start_loc)
     return MPA_ERR_INVALID;
   mpa::AppendArgs a;

@@ -272,6 +272,18 @@ def test_append_block_boundaries(torch_gpu, dtype):
     check_batch(b, f"append block boundaries {dtype}")
 
 
+def test_shared_prefix_block_with_debug_checks(torch_gpu, monkeypatch):
+    """Two sequences share their first (full, read-only) prefix block and
+    append into blocks of their own: MPA_DEBUG=1 accepts the step, and both
+    read the shared keys."""
+    monkeypatch.setenv("MPA_DEBUG", "1")
+    rng = np.random.default_rng(72)
+    b = make_batch([SeqSpec(40, 5), SeqSpec(45, 3), SeqSpec(30, 1)], HeadSpec(8, 2, 128), "bf16", rng)
+    b = dataclasses.replace(b, block_tables=b.block_tables.copy())
+    b.block_tables[1, 0] = b.block_tables[0, 0]
+    check_batch(b, "shared prefix block, MPA_DEBUG=1")
+
+
 def test_decode_only_and_prefill_only(torch_gpu):
     rng = np.random.default_rng(21)
     dec = [SeqSpec(int(c), 1) for c in rng.integers(1, 4000, size=20)]

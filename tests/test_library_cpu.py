@@ -223,3 +223,34 @@ def test_rope_append_rejects_bad_arguments_before_any_launch():
     assert call(128, 99) == mpa.MPA_ERR_INVALID       # position 99 past a 99-row table
     assert call(128, 128, q=None) == mpa.MPA_ERR_INVALID
     assert call(128, 128, table=None) == mpa.MPA_ERR_INVALID
+
+
+def test_debug_append_slot_checks(monkeypatch):
+    """MPA_DEBUG=1: the slots an append writes must be pairwise distinct and
+    must not hold a key that the step reads (shared prefix blocks are
+    read-only); the check needs the host block tables.  Every case here is
+    rejected before any launch."""
+    monkeypatch.setenv("MPA_DEBUG", "1")
+    sh = shape(num_seqs=2, total_q_tokens=3)
+    # sequence 0: 20 keys, appends 1 at position 19 (block 1, slot 3);
+    # sequence 1: 40 keys, appends 2 at positions 38, 39 (block 2, slots 6, 7)
+    sl, qsl = [20, 40], [0, 1, 3]
+    bt = np.arange(16, dtype=np.int32).reshape(2, 8)
+    # no host tables: the check cannot run
+    assert append_rc(sh, sl, qsl) == mpa.MPA_ERR_INVALID
+    # two tokens, one slot: sequence 1 (36 keys) appends positions 34 and 35,
+    # slots 2 and 3 of its block 2, which the table maps onto sequence 0's
+    # block 1, whose slot 3 sequence 0 appends to
+    dup = bt.copy()
+    dup[1, 2] = dup[0, 1]
+    assert append_rc(sh, [20, 36], [0, 1, 3], dup) == mpa.MPA_ERR_INVALID
+    # an append over a key another sequence reads: sequence 1's first block
+    # is sequence 0's last, and sequence 1 reads all 16 of its slots
+    shared = bt.copy()
+    shared[1, 0] = shared[0, 1]
+    assert append_rc(sh, sl, qsl, shared) == mpa.MPA_ERR_INVALID
+    # an append over the appending sequence's own prefix (a table that
+    # repeats a block)
+    own = bt.copy()
+    own[1, 2] = own[1, 0]
+    assert append_rc(sh, sl, qsl, own) == mpa.MPA_ERR_INVALID
