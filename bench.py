@@ -210,6 +210,9 @@ def main(argv=None) -> int:
     ap.add_argument("--kv", default="bf16", choices=("bf16", "fp8"),
                     help="KV-cache element type: bf16 (default) or fp8 (OCP E4M3 codes, one scale per cache; "
                          "queries and outputs stay bf16)")
+    ap.add_argument("--exec", default="serial", choices=("serial", "auto"),
+                    help="auto: run the attention halves as mpa_plan_coexec picks -- one stream, or concurrently "
+                         "on CU-partitioned streams (decode on 1-3 quarters of every XCD)")
     ap.add_argument("--graph", action="store_true",
                     help="also capture one step into a HIP graph (torch.cuda.graph) and time its replays")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -251,6 +254,13 @@ def main(argv=None) -> int:
     has_dec = work["decode_rows"] > 0
     has_pre = work["prefill_chunks"] > 0
     two = args.streams == 2 and has_dec and has_pre
+    coexec_mode = 0
+    if args.exec == "auto":
+        if args.kv != "bf16" or args.streams != 1:
+            raise SystemExit("--exec auto models bf16 caches on the one-stream step")
+        coexec_mode = mpa.plan_coexec(mpa.shape_of(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.scale),
+                                      d.seq_lens_host, d.qsl_host)[0]
+    part = mpa.partition_streams(coexec_mode) if coexec_mode else None
 
     def step(ev=None):
         """append; then prefill half and decode half (concurrently with two
@@ -268,10 +278,14 @@ def main(argv=None) -> int:
         mpa.kv_append(d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
                       d.seq_lens_host, d.qsl_host, stream=stream, **sc)
         mark("append", stream)
-        pre_stream = stream
+        pre_stream = dec_stream = stream
         if two:
             side.wait_stream(stream)
             pre_stream = side
+        if part:
+            dec_stream, pre_stream = part
+            dec_stream.wait_stream(stream)
+            pre_stream.wait_stream(stream)
         if has_pre:
             mpa.prefill_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
                                   d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws, scale=d.scale,
@@ -280,18 +294,22 @@ def main(argv=None) -> int:
         if has_dec:
             mpa.decode_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
                                  d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws, scale=d.scale,
-                                 stream=stream, **sc)
-        mark("decode", stream)
+                                 stream=dec_stream, **sc)
+        mark("decode", dec_stream)
         if two:
             stream.wait_stream(side)
+        if part:
+            stream.wait_stream(dec_stream)
+            stream.wait_stream(pre_stream)
         mark("end", stream)
 
     def new_events(names):
         return {n: torch.cuda.Event(enable_timing=True) for n in names}
 
     # With one stream the halves run prefill-then-decode; with two they overlap.
+    concurrent = two or bool(part)
     spans = {"append": ("start", "append"), "prefill": ("append", "prefill"),
-             "decode": ("prefill", "decode") if not two else ("append", "decode"), "step": ("start", "end")}
+             "decode": ("prefill", "decode") if not concurrent else ("append", "decode"), "step": ("start", "end")}
 
     def avg_ms(evs, span):
         a, b = spans[span]
@@ -358,7 +376,8 @@ def main(argv=None) -> int:
         "config": {"workload": f"{args.config}: {WORKLOADS[args.config]}", "seed": args.seed, "streams": args.streams if two else 1,
                    "kv_cache": "bf16" if args.kv == "bf16" else "fp8 e4m3 (per-cache scale)",
                    "decode_rows": work["decode_rows"], "prefill_chunks": work["prefill_chunks"],
-                   "query_tokens": work["query_tokens"], "parallelism": "single GPU"},
+                   "query_tokens": work["query_tokens"], "parallelism": "single GPU",
+                   "exec": f"decode on {coexec_mode}/4 of every XCD beside prefill" if coexec_mode else "one stream"},
         "roofline": roofline,
         "phases_ms": {k: round(v, 4) for k, v in phase_ms.items()},
         "decode_hbm_gbs": round(dec_gbs, 1) if dec_gbs else None,

@@ -287,7 +287,7 @@ int mpa_get_plan_info(const mpa_shape* shape, const int32_t* seq_lens_host,
  *
  * Rates are in microseconds and GB/s (1e9 bytes/s).  mpa_default_rates
  * fills in figures measured on one MI355X with bench.py.  Only bf16 caches
- * are modelled: MPA_ERR_UNSUPPORTED for f32.
+ * are modelled: MPA_ERR_UNSUPPORTED for f32 and fp8.
  */
 typedef struct {
   double append_fixed_us;
@@ -303,6 +303,13 @@ typedef struct {
   int32_t prefill_slots;
   double append_block_us;
   double append_block_gbs;
+  double coexec_decode_q1;   /* decode half's speed on 1/4 of every XCD's CUs, relative to all */
+  double coexec_decode_q2;   /* ... on 1/2 */
+  double coexec_decode_q3;   /* ... on 3/4 */
+  double coexec_prefill_q1;  /* prefill half's speed on 1/4 of every XCD's CUs, relative to all */
+  double coexec_prefill_q2;  /* ... on 1/2 */
+  double coexec_prefill_q3;  /* ... on 3/4 */
+  double coexec_slowdown;    /* two halves side by side over the slower one alone (>= 1) */
 } mpa_rates;
 
 typedef struct {
@@ -319,6 +326,39 @@ void mpa_default_rates(mpa_rates* rates);
 int mpa_predict_step(const mpa_shape* shape, const int32_t* seq_lens_host,
                      const int32_t* query_start_loc_host, const mpa_rates* rates,
                      mpa_step_time* out);
+
+/*
+ * How to run the step's two attention halves (mpa_decode_attention and
+ * mpa_prefill_attention), chosen per step.  The paper runs spilled prefill
+ * beside decode either as a chunked mixed batch or, in its PDMUX executor,
+ * on a spatial partition of the GPU; both are backends of one executor
+ * interface (section 5).  Here mode 0 runs the halves one after the other
+ * on one stream (as mpa_mixed_paged_attention does); mode k = 1, 2, 3 runs
+ * them concurrently, the decode half on k quarters of every XCD's CUs and
+ * the prefill half on the rest (mpa_partition_streams).  The outputs are
+ * bit-identical in every mode.  The predicted attention time of mode k is
+ *   mode 0: decode + prefill of mpa_predict_step
+ *   mode k: max(decode / coexec_decode_qk, prefill / coexec_prefill_q(4-k))
+ *           * coexec_slowdown
+ * (infinite when the step lacks decode rows or prefill chunks).
+ *
+ * mode          out: the mode with the shortest predicted time
+ * predicted_us  out, may be NULL: double[4], the prediction per mode
+ * Errors as for mpa_predict_step (bf16 caches only).
+ */
+int mpa_plan_coexec(const mpa_shape* shape, const int32_t* seq_lens_host, const int32_t* query_start_loc_host,
+                    const mpa_rates* rates, int32_t* mode, double* predicted_us);
+
+/*
+ * The two streams of partition mode 1..3 on the current device: the decode
+ * half's, restricted to `mode` quarters of every XCD's CUs, and the prefill
+ * half's, restricted to the other CUs.  Created at the first request (per
+ * device and mode, default priority) and kept until the process ends; the
+ * caller orders them against its own stream (events) and never destroys
+ * them.  Returns MPA_ERR_INVALID for another mode, MPA_ERR_HIP when the
+ * runtime refuses.
+ */
+int mpa_partition_streams(int32_t mode, void** decode_stream, void** prefill_stream);
 
 #ifdef __cplusplus
 }

@@ -44,6 +44,8 @@ EXPORTS = (
     "mpa_default_rates",
     "mpa_kv_append_rope",
     "mpa_predict_step",
+    "mpa_plan_coexec",
+    "mpa_partition_streams",
 )
 
 
@@ -101,6 +103,13 @@ class MpaRates(ctypes.Structure):
         ("prefill_slots", ctypes.c_int32),
         ("append_block_us", ctypes.c_double),
         ("append_block_gbs", ctypes.c_double),
+        ("coexec_decode_q1", ctypes.c_double),
+        ("coexec_decode_q2", ctypes.c_double),
+        ("coexec_decode_q3", ctypes.c_double),
+        ("coexec_prefill_q1", ctypes.c_double),
+        ("coexec_prefill_q2", ctypes.c_double),
+        ("coexec_prefill_q3", ctypes.c_double),
+        ("coexec_slowdown", ctypes.c_double),
     ]
 
 
@@ -148,6 +157,12 @@ def lib() -> ctypes.CDLL:
         L.mpa_default_rates.argtypes = [ctypes.POINTER(MpaRates)]
         L.mpa_predict_step.restype = ctypes.c_int
         L.mpa_predict_step.argtypes = [_SHP, _I32P, _I32P, ctypes.POINTER(MpaRates), ctypes.POINTER(MpaStepTime)]
+        L.mpa_plan_coexec.restype = ctypes.c_int
+        L.mpa_plan_coexec.argtypes = [_SHP, _I32P, _I32P, ctypes.POINTER(MpaRates), ctypes.POINTER(ctypes.c_int32),
+                                      ctypes.POINTER(ctypes.c_double)]
+        L.mpa_partition_streams.restype = ctypes.c_int
+        L.mpa_partition_streams.argtypes = [ctypes.c_int32, ctypes.POINTER(ctypes.c_void_p),
+                                            ctypes.POINTER(ctypes.c_void_p)]
         _lib = L
     return _lib
 
@@ -243,6 +258,36 @@ def predict_step(shape: MpaShape, seq_lens_host, qsl_host, rates: Optional[MpaRa
     return out
 
 
+def plan_coexec(shape: MpaShape, seq_lens_host, qsl_host, rates: Optional[MpaRates] = None):
+    """mpa_plan_coexec: (mode, [predicted attention us of modes 0..3])."""
+    sl, qs = _host_i32(seq_lens_host), _host_i32(qsl_host)
+    mode = ctypes.c_int32(-1)
+    pred = (ctypes.c_double * 4)()
+    rc = lib().mpa_plan_coexec(ctypes.byref(shape), _i32p(sl), _i32p(qs),
+                               ctypes.byref(rates) if rates is not None else None, ctypes.byref(mode), pred)
+    if rc != MPA_OK:
+        raise MpaError(rc, "mpa_plan_coexec")
+    return int(mode.value), [float(x) for x in pred]
+
+
+_partition_streams = {}
+
+
+def partition_streams(mode: int):
+    """mpa_partition_streams on the current device, as torch streams
+    (decode half's, prefill half's); cached, never destroyed."""
+    import torch
+
+    key = (torch.cuda.current_device(), int(mode))
+    if key not in _partition_streams:
+        d, p = ctypes.c_void_p(), ctypes.c_void_p()
+        rc = lib().mpa_partition_streams(int(mode), ctypes.byref(d), ctypes.byref(p))
+        if rc != MPA_OK:
+            raise MpaError(rc, "mpa_partition_streams")
+        _partition_streams[key] = (torch.cuda.ExternalStream(d.value), torch.cuda.ExternalStream(p.value))
+    return _partition_streams[key]
+
+
 def workspace_size(shape: MpaShape, seq_lens_host, qsl_host) -> int:
     sl, qs = _host_i32(seq_lens_host), _host_i32(qsl_host)
     return int(lib().mpa_workspace_size(ctypes.byref(shape), _i32p(sl), _i32p(qs)))
@@ -334,3 +379,33 @@ def prefill_attention(q, k_cache, v_cache, block_tables, seq_lens, query_start_l
     """mpa_prefill_attention: only the rows of sequences with q_len > 1."""
     _attention("mpa_prefill_attention", q, k_cache, v_cache, block_tables, seq_lens, query_start_loc,
                seq_lens_host, qsl_host, out, lse, workspace, scale, block_tables_host, stream, k_scale, v_scale)
+
+
+def coexec_attention(q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host, out,
+                     lse=None, workspace=None, scale=None, block_tables_host=None, stream=None, k_scale=1.0,
+                     v_scale=1.0, rates=None, mode=None) -> int:
+    """The step's attention in the mode mpa_plan_coexec picks (or `mode`):
+    0 runs mpa_mixed_paged_attention on `stream`; 1..3 runs the decode and
+    prefill halves concurrently on the partition streams, ordered after
+    `stream` and joined back to it.  Returns the mode used; the outputs are
+    bit-identical in every mode."""
+    import torch
+
+    main = torch.cuda.current_stream() if stream is None else stream
+    kw = dict(lse=lse, workspace=workspace, scale=scale, block_tables_host=block_tables_host, k_scale=k_scale,
+              v_scale=v_scale)
+    if mode is None:
+        shape = shape_of(q, k_cache, block_tables, _host_i32(seq_lens_host), scale, k_scale, v_scale)
+        mode, _ = plan_coexec(shape, seq_lens_host, qsl_host, rates)
+    args = (q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host, out)
+    if mode == 0:
+        mixed_paged_attention(*args, stream=main, **kw)
+        return 0
+    ds, ps = partition_streams(mode)
+    ds.wait_stream(main)
+    ps.wait_stream(main)
+    decode_attention(*args, stream=ds, **kw)
+    prefill_attention(*args, stream=ps, **kw)
+    main.wait_stream(ds)
+    main.wait_stream(ps)
+    return int(mode)

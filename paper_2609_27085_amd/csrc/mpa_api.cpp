@@ -1,6 +1,7 @@
 // C ABI of the mixed paged-attention library: host-side validation, the
 // varlen planner (decode rows -> split-K work items, prefill chunks -> query
 // tiles) and the launch sequence.  Every check runs before the first launch.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -9,6 +10,7 @@
 
 #include <algorithm>
 #include <functional>
+#include <mutex>
 #include <queue>
 #include <unordered_set>
 #include <vector>
@@ -19,6 +21,7 @@
 namespace {
 
 using mpa::kBlock;
+constexpr int kMaskWords = 8;  // CU-mask words: devices of up to 256 CUs
 
 struct Batch {
   std::vector<int> decode;   // sequence ids with q_len == 1
@@ -157,7 +160,8 @@ size_t workspace_bytes(const mpa_shape* sh, long items) {
 // small token budget, on long cached prefixes) each chunk's prefix is divided
 // among up to `want` splits of about kPrefillMinSplitTiles 64-key tiles or
 // more; the last split also takes the chunk's own keys (and the causal
-// diagonal), so every split holds keys of every row.  bf16 only.
+// diagonal), so every split holds keys of every row.  bf16 and fp8 caches
+// (the MFMA kernel); f32 chunks are not split.
 struct PrefillSplit {
   int nsplit = 1;
   int tiles = 0;        // 64-key tiles of every split but the last
@@ -310,83 +314,11 @@ int run_append(const mpa_shape* shape, const void* k_new, const void* v_new, voi
 
 }  // namespace
 
-extern "C" {
+namespace {
 
-const char* mpa_status_string(int status) {
-  switch (status) {
-    case MPA_OK: return "ok";
-    case MPA_ERR_INVALID: return "invalid argument or batch metadata";
-    case MPA_ERR_UNSUPPORTED: return "unsupported shape or dtype";
-    case MPA_ERR_WORKSPACE: return "workspace missing or too small";
-    case MPA_ERR_HIP: return "HIP launch error";
-    default: return "unknown status";
-  }
-}
-
-int mpa_get_plan_info(const mpa_shape* shape, const int32_t* seq_lens_host, const int32_t* qsl_host,
-                      mpa_plan_info* info) {
-  if (!info) return MPA_ERR_INVALID;
-  Batch b;
-  int rc = check_batch(shape, seq_lens_host, qsl_host, nullptr, false, &b);
-  if (rc != MPA_OK) return rc;
-  const int split = choose_split(shape, b, seq_lens_host);
-  info->num_decode_seqs = (int32_t)b.decode.size();
-  info->num_prefill_seqs = (int32_t)b.prefill.size();
-  info->split_tokens = split;
-  info->num_decode_items = (int32_t)decode_items(shape, b, seq_lens_host, split);
-  long tiles = 0;
-  const int qt = q_tile(shape);
-  const std::vector<PrefillSplit> ps =
-      prefill_splits(shape, b, seq_lens_host, qsl_host, decode_items(shape, b, seq_lens_host, split));
-  int max_split = b.prefill.empty() ? 0 : 1;
-  for (size_t k = 0; k < b.prefill.size(); ++k) {
-    const int s = b.prefill[k];
-    tiles += (long)(qsl_host[s + 1] - qsl_host[s] + qt - 1) / qt * ps[k].nsplit;
-    max_split = std::max(max_split, ps[k].nsplit);
-  }
-  info->num_prefill_tiles = (int32_t)(tiles * shape->num_kv_heads);
-  info->prefill_max_splits = max_split;
-  info->decode_launches = (int32_t)((b.decode.size() + mpa::kMaxPlanSeqs - 1) / mpa::kMaxPlanSeqs);
-  return MPA_OK;
-}
-
-void mpa_default_rates(mpa_rates* r) {
-  if (!r) return;
-  // Least-squares fit (log error) to the phase times bench.py measured on
-  // one MI355X for decode8b, lent, agentic, budget0/256/1024/4096 and
-  // longctx (seed 0, each phase less the ~5 us of its event record); the
-  // merge, few-key and wave figures are single kernel times from rocprofv3.
-  // The append figures are fitted to the append phases alone: the
-  // per-token launch from decode8b and budget0, the per-block launch (a
-  // latency floor, then about 3.7 TB/s) from lent, budget4096 and longctx.
-  r->append_fixed_us = 3.9;
-  r->append_gbs = 545.0;
-  r->append_block_us = 17.0;
-  r->append_block_gbs = 3700.0;
-  r->decode_fixed_us = 2.0;
-  r->decode_gbs = 5600.0;
-  r->decode_wave_gbs = 4.8;
-  r->merge_us = 5.0;
-  r->prefill_wg_us = 18.0;
-  r->prefill_tile_us = 1.85;
-  r->prefill_merge_us = 5.0;
-  r->prefill_fixup_us = 8.0;
-  r->prefill_slots = 256;
-}
-
-int mpa_predict_step(const mpa_shape* shape, const int32_t* seq_lens_host, const int32_t* qsl_host,
-                     const mpa_rates* rates, mpa_step_time* out) {
-  if (!out) return MPA_ERR_INVALID;
-  Batch b;
-  int rc = check_batch(shape, seq_lens_host, qsl_host, nullptr, false, &b);
-  if (rc != MPA_OK) return rc;
-  if (shape->dtype != MPA_BF16) return MPA_ERR_UNSUPPORTED;
-  mpa_rates def;
-  mpa_default_rates(&def);
-  const mpa_rates& r = rates ? *rates : def;
-  if (!(r.append_gbs > 0) || !(r.append_block_gbs > 0) || !(r.decode_gbs > 0) || !(r.decode_wave_gbs > 0) ||
-      r.prefill_slots <= 0)
-    return MPA_ERR_INVALID;
+// The step-time model (mpa_predict_step), shared with the mode planner.
+mpa_step_time model_step(const mpa_shape* shape, const Batch& b, const int32_t* seq_lens_host,
+                         const int32_t* qsl_host, const mpa_rates& r) {
   const double elem = 2.0;  // bf16
   const double row_bytes = (double)shape->num_kv_heads * shape->head_dim * elem;  // one token's K (or V)
   mpa_step_time t = {0.0, 0.0, 0.0, 0.0};
@@ -461,7 +393,173 @@ int mpa_predict_step(const mpa_shape* shape, const int32_t* seq_lens_host, const
   }
   if (few) t.prefill_us += r.prefill_fixup_us;
   t.step_us = t.append_us + t.decode_us + t.prefill_us;
-  *out = t;
+  return t;
+}
+
+int check_model_inputs(const mpa_shape* shape, const int32_t* seq_lens_host, const int32_t* qsl_host,
+                       const mpa_rates& r, Batch* b) {
+  int rc = check_batch(shape, seq_lens_host, qsl_host, nullptr, false, b);
+  if (rc != MPA_OK) return rc;
+  if (shape->dtype != MPA_BF16) return MPA_ERR_UNSUPPORTED;
+  if (!(r.append_gbs > 0) || !(r.append_block_gbs > 0) || !(r.decode_gbs > 0) || !(r.decode_wave_gbs > 0) ||
+      r.prefill_slots <= 0)
+    return MPA_ERR_INVALID;
+  return MPA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mpa_status_string(int status) {
+  switch (status) {
+    case MPA_OK: return "ok";
+    case MPA_ERR_INVALID: return "invalid argument or batch metadata";
+    case MPA_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+    case MPA_ERR_WORKSPACE: return "workspace missing or too small";
+    case MPA_ERR_HIP: return "HIP launch error";
+    default: return "unknown status";
+  }
+}
+
+int mpa_get_plan_info(const mpa_shape* shape, const int32_t* seq_lens_host, const int32_t* qsl_host,
+                      mpa_plan_info* info) {
+  if (!info) return MPA_ERR_INVALID;
+  Batch b;
+  int rc = check_batch(shape, seq_lens_host, qsl_host, nullptr, false, &b);
+  if (rc != MPA_OK) return rc;
+  const int split = choose_split(shape, b, seq_lens_host);
+  info->num_decode_seqs = (int32_t)b.decode.size();
+  info->num_prefill_seqs = (int32_t)b.prefill.size();
+  info->split_tokens = split;
+  info->num_decode_items = (int32_t)decode_items(shape, b, seq_lens_host, split);
+  long tiles = 0;
+  const int qt = q_tile(shape);
+  const std::vector<PrefillSplit> ps =
+      prefill_splits(shape, b, seq_lens_host, qsl_host, decode_items(shape, b, seq_lens_host, split));
+  int max_split = b.prefill.empty() ? 0 : 1;
+  for (size_t k = 0; k < b.prefill.size(); ++k) {
+    const int s = b.prefill[k];
+    tiles += (long)(qsl_host[s + 1] - qsl_host[s] + qt - 1) / qt * ps[k].nsplit;
+    max_split = std::max(max_split, ps[k].nsplit);
+  }
+  info->num_prefill_tiles = (int32_t)(tiles * shape->num_kv_heads);
+  info->prefill_max_splits = max_split;
+  info->decode_launches = (int32_t)((b.decode.size() + mpa::kMaxPlanSeqs - 1) / mpa::kMaxPlanSeqs);
+  return MPA_OK;
+}
+
+void mpa_default_rates(mpa_rates* r) {
+  if (!r) return;
+  // Least-squares fit (log error) to the phase times bench.py measured on
+  // one MI355X for decode8b, lent, agentic, budget0/256/1024/4096 and
+  // longctx (seed 0, each phase less the ~5 us of its event record); the
+  // merge, few-key and wave figures are single kernel times from rocprofv3.
+  // The append figures are fitted to the append phases alone: the
+  // per-token launch from decode8b and budget0, the per-block launch (a
+  // latency floor, then about 3.7 TB/s) from lent, budget4096 and longctx.
+  r->append_fixed_us = 3.9;
+  r->append_gbs = 545.0;
+  r->append_block_us = 17.0;
+  r->append_block_gbs = 3700.0;
+  r->decode_fixed_us = 2.0;
+  r->decode_gbs = 5600.0;
+  r->decode_wave_gbs = 4.8;
+  r->merge_us = 5.0;
+  r->prefill_wg_us = 18.0;
+  r->prefill_tile_us = 1.85;
+  r->prefill_merge_us = 5.0;
+  r->prefill_fixup_us = 8.0;
+  r->prefill_slots = 256;
+  // CU-partitioned co-execution (mpa_plan_coexec), measured on agentic, lent
+  // and budget4096, each half alone on its CU set: the decode half's speed
+  // on 1, 2 and 3 quarters of every XCD's CUs relative to the whole device,
+  // the prefill half's likewise (faster than its share of the CUs: fewer
+  // CUs contend for the same HBM and L2), and the slowdown of the two halves
+  // side by side over the slower of them alone (shared HBM, L2 and MALL;
+  // 1.09-1.42 across the nine partitions, the decisions checked against all
+  // of them)
+  r->coexec_decode_q1 = 0.54;
+  r->coexec_decode_q2 = 0.85;
+  r->coexec_decode_q3 = 1.0;
+  r->coexec_prefill_q1 = 0.335;
+  r->coexec_prefill_q2 = 0.62;
+  r->coexec_prefill_q3 = 0.77;
+  r->coexec_slowdown = 1.25;
+}
+
+int mpa_predict_step(const mpa_shape* shape, const int32_t* seq_lens_host, const int32_t* qsl_host,
+                     const mpa_rates* rates, mpa_step_time* out) {
+  if (!out) return MPA_ERR_INVALID;
+  mpa_rates def;
+  mpa_default_rates(&def);
+  const mpa_rates& r = rates ? *rates : def;
+  Batch b;
+  int rc = check_model_inputs(shape, seq_lens_host, qsl_host, r, &b);
+  if (rc != MPA_OK) return rc;
+  *out = model_step(shape, b, seq_lens_host, qsl_host, r);
+  return MPA_OK;
+}
+
+int mpa_plan_coexec(const mpa_shape* shape, const int32_t* seq_lens_host, const int32_t* qsl_host,
+                    const mpa_rates* rates, int32_t* mode, double* predicted_us) {
+  if (!mode) return MPA_ERR_INVALID;
+  mpa_rates def;
+  mpa_default_rates(&def);
+  const mpa_rates& r = rates ? *rates : def;
+  Batch b;
+  int rc = check_model_inputs(shape, seq_lens_host, qsl_host, r, &b);
+  if (rc != MPA_OK) return rc;
+  const double dfrac[4] = {1.0, r.coexec_decode_q1, r.coexec_decode_q2, r.coexec_decode_q3};
+  const double pfrac[4] = {1.0, r.coexec_prefill_q3, r.coexec_prefill_q2, r.coexec_prefill_q1};
+  if (!(r.coexec_slowdown >= 1.0)) return MPA_ERR_INVALID;
+  for (int k = 1; k <= 3; ++k)
+    if (!(dfrac[k] > 0) || !(pfrac[k] > 0)) return MPA_ERR_INVALID;
+  const mpa_step_time serial = model_step(shape, b, seq_lens_host, qsl_host, r);
+  double t[4];
+  t[0] = serial.decode_us + serial.prefill_us;
+  for (int k = 1; k <= 3; ++k)
+    t[k] = b.decode.empty() || b.prefill.empty()
+               ? INFINITY  // nothing to overlap
+               : std::max(serial.decode_us / dfrac[k], serial.prefill_us / pfrac[k]) * r.coexec_slowdown;
+  int best = 0;
+  for (int k = 1; k <= 3; ++k)
+    if (t[k] < t[best]) best = k;
+  *mode = best;
+  if (predicted_us)
+    for (int k = 0; k < 4; ++k) predicted_us[k] = t[k];
+  return MPA_OK;
+}
+
+int mpa_partition_streams(int32_t mode, void** decode_stream, void** prefill_stream) {
+  if (mode < 1 || mode > 3 || !decode_stream || !prefill_stream) return MPA_ERR_INVALID;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return MPA_ERR_HIP;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0 ||
+      cus > 32 * kMaskWords)
+    return MPA_ERR_HIP;
+  static std::mutex lock;
+  static hipStream_t made[64][3][2];
+  std::lock_guard<std::mutex> guard(lock);
+  hipStream_t* pair = made[dev][mode - 1];
+  if (!pair[0]) {
+    // CU i (the mask's numbering) goes to the decode half when (i / 8) % 4 <
+    // mode: `mode` quarters of every XCD whether the numbering runs XCD by
+    // XCD or interleaves them
+    uint32_t dmask[kMaskWords] = {0}, pmask[kMaskWords] = {0};
+    for (int i = 0; i < cus; ++i) ((i / 8) % 4 < mode ? dmask : pmask)[i / 32] |= 1u << (i % 32);
+    const uint32_t words = (uint32_t)((cus + 31) / 32);
+    hipStream_t d = nullptr, p = nullptr;
+    if (hipExtStreamCreateWithCUMask(&d, words, dmask) != hipSuccess) return MPA_ERR_HIP;
+    if (hipExtStreamCreateWithCUMask(&p, words, pmask) != hipSuccess) {
+      (void)hipStreamDestroy(d);
+      return MPA_ERR_HIP;
+    }
+    pair[0] = d;
+    pair[1] = p;
+  }
+  *decode_stream = pair[0];
+  *prefill_stream = pair[1];
   return MPA_OK;
 }
 

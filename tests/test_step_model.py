@@ -154,3 +154,62 @@ def test_decode_rows_split_into_equal_block_aligned_parts(L):
     r = unit_rates(decode_gbs=1e12, decode_wave_gbs=1.0)
     t = predict([9000], rates=r)
     assert math.isclose(t.decode_us, part * 2 * 128 * 2 / 1e3, rel_tol=1e-12)
+
+
+def test_coexec_plan_formula_and_choice(L):
+    """mpa_plan_coexec: mode 0 is the serial decode + prefill of the model;
+    mode k is max(decode / decode speed on k quarters, prefill / prefill
+    speed on the other quarters) times the side-by-side slowdown; the
+    shortest wins (the lowest mode on a tie)."""
+    sl, qsl = batch([6000] * 64, [(1024, 4096)])
+    sh = shape(sl, qsl)
+    r = mpa.default_rates()
+    st = mpa.predict_step(sh, sl, qsl, r)
+    mode, pred = mpa.plan_coexec(sh, sl, qsl, r)
+    assert math.isclose(pred[0], st.decode_us + st.prefill_us, rel_tol=1e-12)
+    dq = [r.coexec_decode_q1, r.coexec_decode_q2, r.coexec_decode_q3]
+    pq = [r.coexec_prefill_q3, r.coexec_prefill_q2, r.coexec_prefill_q1]
+    for k in (1, 2, 3):
+        want = max(st.decode_us / dq[k - 1], st.prefill_us / pq[k - 1]) * r.coexec_slowdown
+        assert math.isclose(pred[k], want, rel_tol=1e-12)
+    assert mode == int(np.argmin(pred))
+    # free overlap (no slowdown, full speed on any share): partition wins, mode 1 first
+    for f in ("coexec_decode_q1", "coexec_decode_q2", "coexec_decode_q3", "coexec_prefill_q1",
+              "coexec_prefill_q2", "coexec_prefill_q3", "coexec_slowdown"):
+        setattr(r, f, 1.0)
+    mode, pred = mpa.plan_coexec(sh, sl, qsl, r)
+    assert mode == 1 and pred[1] == pred[2] == pred[3] < pred[0]
+    # a step with nothing to overlap stays serial
+    sl2, qsl2 = batch([6000] * 8)
+    mode, pred = mpa.plan_coexec(shape(sl2, qsl2), sl2, qsl2)
+    assert mode == 0 and all(math.isinf(x) for x in pred[1:])
+    # bad rates
+    r.coexec_slowdown = 0.5
+    with pytest.raises(mpa.MpaError):
+        mpa.plan_coexec(sh, sl, qsl, r)
+
+
+def test_coexec_plan_on_the_workloads(L):
+    """With the measured rates the planner picks, for the eight workloads at
+    seed 0, the execution the measurements favoured: the decode half on a
+    quarter of the CUs beside the agentic prefill, on three quarters beside
+    the 4096-token budget chunk, and one stream everywhere else."""
+    from workloads.configs import config_specs
+
+    want = {"decode8b": 0, "lent": 0, "agentic": 1, "budget0": 0, "budget256": 0, "budget1024": 0,
+            "budget4096": 3, "longctx": 0}
+    for cfg, mode in want.items():
+        specs, heads, _, _ = config_specs(cfg, 0)
+        sl = np.asarray([sp.ctx for sp in specs], np.int32)
+        qsl = np.concatenate([[0], np.cumsum([sp.q_len for sp in specs])]).astype(np.int32)
+        sh = shape(sl, qsl, hq=heads.num_q_heads, hkv=heads.num_kv_heads, d=heads.head_dim)
+        assert mpa.plan_coexec(sh, sl, qsl)[0] == mode, cfg
+
+
+def test_partition_streams_arguments(L):
+    import ctypes
+
+    d, p = ctypes.c_void_p(), ctypes.c_void_p()
+    for bad in (0, 4, -1):
+        assert L.mpa_partition_streams(bad, ctypes.byref(d), ctypes.byref(p)) == mpa.MPA_ERR_INVALID
+    assert L.mpa_partition_streams(1, None, ctypes.byref(p)) == mpa.MPA_ERR_INVALID
