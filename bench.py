@@ -20,6 +20,8 @@ before timing starts.  Prints one JSON line:
                  FLOPs at 2.5 PF
   model_ms       the library's step-time model (mpa_predict_step) for the batch
   graph          (--graph) step time when the step is replayed from a HIP graph
+  measured_peaks what the library's probes sustain on this device (HBM stream
+                 read, dense bf16 MFMA) and the roofline's fraction of that
   cpu_baseline   the CPU oracle, timed on a bounded sample of the same step
 
     python bench.py [--steps K] [--warmup W] [--config decode8b] [--seed 0]
@@ -195,6 +197,36 @@ def cpu_baseline(d, budget_s: float, seed: int):
     }
 
 
+def measured_peaks(torch, mpa, read_bytes: int = 2 << 30, mfma_iters: int = 20000, reps: int = 5) -> dict:
+    """The library's probes (mpa_probe_stream_read, mpa_probe_mfma_bf16),
+    median of `reps` launches after two untimed ones: HBM read GB/s over a
+    buffer 8x the 256 MB last-level cache, and dense bf16 MFMA TFLOP/s."""
+    buf = torch.empty(read_bytes, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(4, dtype=torch.float32, device="cuda")
+
+    def timed(launch):
+        for _ in range(2):
+            launch()
+        ms = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            launch()
+            b.record()
+            b.synchronize()
+            ms.append(a.elapsed_time(b))
+        return float(np.median(ms))
+
+    read_ms = timed(lambda: mpa.probe_stream_read(buf, sink))
+    flops = []
+    mfma_ms = timed(lambda: flops.append(mpa.probe_mfma_bf16(mfma_iters, sink)))
+    del buf
+    return {"stream_read_gbs": round(read_bytes / (read_ms * 1e-3) / 1e9, 1),
+            "mfma_bf16_tflops": round(flops[-1] / (mfma_ms * 1e-3) / 1e12, 1),
+            "how": f"median of {reps}: one {read_bytes >> 20} MiB read with 16-byte loads; "
+                   f"{mfma_iters} rounds of 4 independent 32x32x16 bf16 MFMAs in 4096 waves"}
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -204,6 +236,8 @@ def main(argv=None) -> int:
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-probes", action="store_true",
+                    help="skip the measured-peak probes (HBM stream read, bf16 MFMA) after the timed steps")
     ap.add_argument("--streams", type=int, default=1, choices=(1, 2),
                     help="2: the decode and prefill halves of the step run concurrently on two streams "
                          "(the library's mpa_decode_attention / mpa_prefill_attention); 1 (default): one after the other")
@@ -213,6 +247,9 @@ def main(argv=None) -> int:
     ap.add_argument("--exec", default="serial", choices=("serial", "auto"),
                     help="auto: run the attention halves as mpa_plan_coexec picks -- one stream, or concurrently "
                          "on CU-partitioned streams (decode on 1-3 quarters of every XCD)")
+    ap.add_argument("--tp", type=int, default=1, choices=(1, 2, 4, 8),
+                    help="run one GPU's share of a tp-way tensor-parallel layout: the same sequences with "
+                         "1/tp of the query and KV heads (the paper's decode workers run TP4)")
     ap.add_argument("--graph", action="store_true",
                     help="also capture one step into a HIP graph (torch.cuda.graph) and time its replays")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -242,7 +279,7 @@ def main(argv=None) -> int:
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     mpa.lib()
-    specs, heads, nb, rng = config_specs(args.config, args.seed)
+    specs, heads, nb, rng = config_specs(args.config, args.seed, tp=args.tp)
     d = device_step(specs, heads, args.kv, rng, args.seed, num_blocks=nb)
     work = algorithmic_work(d.seq_lens_host, d.qsl_host, heads.num_q_heads, heads.num_kv_heads, heads.head_dim, 2,
                             kv_bytes=1 if args.kv == "fp8" else 2)
@@ -353,7 +390,7 @@ def main(argv=None) -> int:
         "peak": peak,
         "unit": unit,
         "frac": round(achieved / peak, 4),
-        "traffic": measured_traffic(args.config, dom) if args.kv == "bf16" else None,
+        "traffic": measured_traffic(args.config, dom) if args.kv == "bf16" and args.tp == 1 else None,
         "kernel": kernel,
         "phase_ms": round(dom_ms, 4),
         "algorithmic_per_launch": work[f"{dom}_bytes"] if dom == "decode" else work["prefill_flops"],
@@ -373,10 +410,14 @@ def main(argv=None) -> int:
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) values, shuffled block tables)",
-        "config": {"workload": f"{args.config}: {WORKLOADS[args.config]}", "seed": args.seed, "streams": args.streams if two else 1,
+        "config": {"workload": f"{args.config}: {WORKLOADS[args.config]}"
+                               + (f"; one GPU's share of TP{args.tp}: {heads.num_q_heads}/{heads.num_kv_heads} heads"
+                                  if args.tp > 1 else ""),
+                   "seed": args.seed, "streams": args.streams if two else 1,
                    "kv_cache": "bf16" if args.kv == "bf16" else "fp8 e4m3 (per-cache scale)",
                    "decode_rows": work["decode_rows"], "prefill_chunks": work["prefill_chunks"],
-                   "query_tokens": work["query_tokens"], "parallelism": "single GPU",
+                   "query_tokens": work["query_tokens"],
+                   "parallelism": f"one GPU's share of tp{args.tp}" if args.tp > 1 else "single GPU",
                    "exec": f"decode on {coexec_mode}/4 of every XCD beside prefill" if coexec_mode else "one stream"},
         "roofline": roofline,
         "phases_ms": {k: round(v, 4) for k, v in phase_ms.items()},
@@ -395,6 +436,11 @@ def main(argv=None) -> int:
     line["step_roofline"] = {"t_mem_ms": round(t_mem * 1e3, 4), "t_mfma_ms": round(t_mfma * 1e3, 4),
                              "max_frac": round(max(t_mem, t_mfma) / t_step, 4),
                              "sum_frac": round((t_mem + t_mfma) / t_step, 4)}
+    if not args.no_probes:
+        peaks = measured_peaks(torch, mpa)
+        meas = peaks["stream_read_gbs"] if dom == "decode" else peaks["mfma_bf16_tflops"]
+        peaks["roofline_frac_of_measured"] = round(achieved / meas, 4)
+        line["measured_peaks"] = peaks
     # the library's step-time model (mpa_predict_step; bf16 caches) for this batch
     if args.kv == "bf16":
         pred = mpa.predict_step(mpa.shape_of(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.scale),

@@ -88,7 +88,7 @@ typedef enum {
   MPA_OK = 0,
   MPA_ERR_INVALID = -1,     /* malformed arguments or batch metadata */
   MPA_ERR_UNSUPPORTED = -2, /* a shape or dtype this build does not handle */
-  MPA_ERR_WORKSPACE = -3,   /* workspace missing or smaller than required */
+  MPA_ERR_WORKSPACE = -3,   /* workspace missing, smaller than required or misaligned */
   MPA_ERR_HIP = -4          /* a HIP launch reported an error */
 } mpa_status;
 
@@ -202,7 +202,8 @@ size_t mpa_workspace_size(const mpa_shape* shape, const int32_t* seq_lens_host,
  * out               device [T][Hq][d], written for every row of every
  *                   sequence with q_len > 0
  * lse               device [T][Hq] float32, or NULL
- * workspace         device scratch of at least mpa_workspace_size() bytes
+ * workspace         device scratch of at least mpa_workspace_size() bytes,
+ *                   16-byte aligned
  *                   (may be NULL when that is 0); contents on entry unused
  * Other arguments as for mpa_kv_append.
  */
@@ -281,9 +282,11 @@ int mpa_get_plan_info(const mpa_shape* shape, const int32_t* seq_lens_host,
  *             launch when a row is split
  *   prefill = per launch: the makespan of its workgroups, each taking
  *             prefill_wg_us + prefill_tile_us per 64-key tile, dealt in
- *             launch order to prefill_slots workgroup slots; plus
- *             prefill_merge_us when a chunk is KV-split and prefill_fixup_us
- *             when a chunk sits on a prefix shorter than 64 tokens
+ *             launch order to prefill_slots workgroup slots; plus, per
+ *             launch with a KV-split chunk, prefill_merge_us +
+ *             prefill_merge_row_us per partial (token, q head, split) row;
+ *             plus prefill_fixup_us when a chunk sits on a prefix shorter
+ *             than 64 tokens
  *
  * Rates are in microseconds and GB/s (1e9 bytes/s).  mpa_default_rates
  * fills in figures measured on one MI355X with bench.py.  Only bf16 caches
@@ -310,6 +313,7 @@ typedef struct {
   double coexec_prefill_q2;  /* ... on 1/2 */
   double coexec_prefill_q3;  /* ... on 3/4 */
   double coexec_slowdown;    /* two halves side by side over the slower one alone (>= 1) */
+  double prefill_merge_row_us; /* KV-split merge, per partial (token, q head, split) row */
 } mpa_rates;
 
 typedef struct {
@@ -359,6 +363,28 @@ int mpa_plan_coexec(const mpa_shape* shape, const int32_t* seq_lens_host, const 
  * runtime refuses.
  */
 int mpa_partition_streams(int32_t mode, void** decode_stream, void** prefill_stream);
+
+/*
+ * Measurement probes (not part of the attention path).  They measure the
+ * device's sustained rate on the two resources the step is bound by:
+ * decode rows on HBM reads, prefill chunks on dense bf16 matrix-core work
+ * (the paper's split of decode as memory bound and prefill as compute
+ * bound, section 2.1), so that a kernel's rate can also be stated against a
+ * measured peak.  Both launch one kernel on `stream`, allocate nothing, and
+ * return MPA_OK, MPA_ERR_INVALID (nothing launched) or MPA_ERR_HIP.
+ *
+ * mpa_probe_stream_read: reads every byte of buf once with 16-byte loads.
+ *   buf    device, 16-byte aligned, `bytes` long (a multiple of 16, > 0)
+ *   sink   device uint32_t[1]; written only when the data's XOR hits one
+ *          fixed value (it keeps the loads), so its contents are unspecified
+ *
+ * mpa_probe_mfma_bf16: 1,024 workgroups of four waves (four per SIMD), each
+ *   wave running `iters` rounds of four independent 32x32x16 bf16 MFMAs.
+ *   sink   device float[1], never written in practice
+ *   flops  host out, may be NULL: the launch's multiply-add work, 2 flops each
+ */
+int mpa_probe_stream_read(const void* buf, size_t bytes, uint32_t* sink, void* stream);
+int mpa_probe_mfma_bf16(int32_t iters, float* sink, double* flops, void* stream);
 
 #ifdef __cplusplus
 }

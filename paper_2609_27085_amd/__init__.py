@@ -46,6 +46,8 @@ EXPORTS = (
     "mpa_predict_step",
     "mpa_plan_coexec",
     "mpa_partition_streams",
+    "mpa_probe_stream_read",
+    "mpa_probe_mfma_bf16",
 )
 
 
@@ -110,6 +112,7 @@ class MpaRates(ctypes.Structure):
         ("coexec_prefill_q2", ctypes.c_double),
         ("coexec_prefill_q3", ctypes.c_double),
         ("coexec_slowdown", ctypes.c_double),
+        ("prefill_merge_row_us", ctypes.c_double),
     ]
 
 
@@ -163,6 +166,10 @@ def lib() -> ctypes.CDLL:
         L.mpa_partition_streams.restype = ctypes.c_int
         L.mpa_partition_streams.argtypes = [ctypes.c_int32, ctypes.POINTER(ctypes.c_void_p),
                                             ctypes.POINTER(ctypes.c_void_p)]
+        L.mpa_probe_stream_read.restype = ctypes.c_int
+        L.mpa_probe_stream_read.argtypes = [_P, ctypes.c_size_t, _P, _P]
+        L.mpa_probe_mfma_bf16.restype = ctypes.c_int
+        L.mpa_probe_mfma_bf16.argtypes = [ctypes.c_int32, _P, ctypes.POINTER(ctypes.c_double), _P]
         _lib = L
     return _lib
 
@@ -286,6 +293,23 @@ def partition_streams(mode: int):
             raise MpaError(rc, "mpa_partition_streams")
         _partition_streams[key] = (torch.cuda.ExternalStream(d.value), torch.cuda.ExternalStream(p.value))
     return _partition_streams[key]
+
+
+def probe_stream_read(buf, sink, stream=None) -> None:
+    """mpa_probe_stream_read over the bytes of the contiguous device tensor
+    buf; sink: a device tensor of at least 4 bytes."""
+    rc = lib().mpa_probe_stream_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), _stream(stream))
+    if rc != MPA_OK:
+        raise MpaError(rc, "mpa_probe_stream_read")
+
+
+def probe_mfma_bf16(iters: int, sink, stream=None) -> float:
+    """mpa_probe_mfma_bf16; returns the launch's FLOPs."""
+    flops = ctypes.c_double()
+    rc = lib().mpa_probe_mfma_bf16(int(iters), _ptr(sink), ctypes.byref(flops), _stream(stream))
+    if rc != MPA_OK:
+        raise MpaError(rc, "mpa_probe_mfma_bf16")
+    return flops.value
 
 
 def workspace_size(shape: MpaShape, seq_lens_host, qsl_host) -> int:

@@ -105,7 +105,7 @@ RowSplit row_split(int L, int S) {
 // splits fill the last round of waves; fewer, larger ones cut start-up and
 // merge work).  MPA_SPLIT_TOKENS (a multiple of 16, at most 1024) overrides
 // it for tuning sweeps.
-int choose_split(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens) {
+int choose_split_uncached(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens) {
   if (const char* env = getenv("MPA_SPLIT_TOKENS")) {
     const int v = atoi(env);
     if (v >= kBlock && v <= 1024 && v % kBlock == 0) return v;
@@ -126,6 +126,49 @@ int choose_split(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens) {
     }
   }
   return best;
+}
+
+// Per-thread memo of the last batch's two plan choices (the decode split
+// and the prefill split count).  One step plans its batch several times --
+// workspace sizing, the append, each attention half, the step model -- and
+// the searches behind the choices cost more host time than the rest of the
+// plan.  The key is everything the choices depend on: the shape's heads,
+// head_dim and dtype, the exact seq_lens and query_start_loc, the device
+// (its wave capacity) and the tuning overrides in the environment.
+struct PlanMemo {
+  int32_t key[7] = {-1, -1, -1, -1, -1, -1, -1};
+  std::vector<int32_t> seq_lens, qsl;
+  int split = 0;  // 0: not chosen yet
+  int want = 0;
+};
+
+int env_int(const char* name) {
+  const char* e = getenv(name);
+  return e ? atoi(e) : -1;
+}
+
+PlanMemo& plan_memo(const mpa_shape* sh, const int32_t* seq_lens, const int32_t* qsl) {
+  thread_local PlanMemo m;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) dev = -1;
+  const int32_t key[7] = {sh->num_q_heads, sh->num_kv_heads, sh->head_dim, (int32_t)sh->dtype, dev,
+                          env_int("MPA_SPLIT_TOKENS"), env_int("MPA_PREFILL_SPLITS")};
+  const size_t n = (size_t)sh->num_seqs;
+  if (memcmp(key, m.key, sizeof key) != 0 || m.seq_lens.size() != n || m.qsl.size() != n + 1 ||
+      (n && memcmp(m.seq_lens.data(), seq_lens, n * sizeof(int32_t)) != 0) ||
+      memcmp(m.qsl.data(), qsl, (n + 1) * sizeof(int32_t)) != 0) {
+    memcpy(m.key, key, sizeof key);
+    m.seq_lens.assign(seq_lens, seq_lens + n);
+    m.qsl.assign(qsl, qsl + n + 1);
+    m.split = m.want = 0;
+  }
+  return m;
+}
+
+int choose_split(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens, const int32_t* qsl) {
+  PlanMemo& m = plan_memo(sh, seq_lens, qsl);
+  if (m.split == 0) m.split = choose_split_uncached(sh, b, seq_lens);
+  return m.split;
 }
 
 long decode_items(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens, int split) {
@@ -155,28 +198,21 @@ size_t workspace_bytes(const mpa_shape* sh, long items) {
 }
 
 // KV splits of the prefill chunks.  A chunk's query tiles times the KV heads
-// are its workgroups, and each workgroup holds a whole CU.  When the batch
-// has fewer than kPrefillSplitTarget of them (short chunks, e.g. a lease's
-// small token budget, on long cached prefixes) each chunk's prefix is divided
-// among up to `want` splits of about kPrefillMinSplitTiles 64-key tiles or
-// more; the last split also takes the chunk's own keys (and the causal
-// diagonal), so every split holds keys of every row.  bf16 and fp8 caches
-// (the MFMA kernel); f32 chunks are not split.
+// are its workgroups, and each workgroup holds a whole CU.  With `want`
+// splits, each chunk's cached prefix is divided among up to `want` parts of
+// kPrefillMinSplitTiles 64-key tiles or more; the last split also takes the
+// chunk's own keys (and the causal diagonal), so every split holds keys of
+// every row.  bf16 and fp8 caches (the MFMA kernel); f32 chunks are not
+// split.
 struct PrefillSplit {
   int nsplit = 1;
   int tiles = 0;        // 64-key tiles of every split but the last
   long item_base = 0;   // first workspace slot of the chunk's partials
 };
 
-std::vector<PrefillSplit> prefill_splits(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens,
-                                         const int32_t* qsl, long first_item) {
+std::vector<PrefillSplit> split_layout(const Batch& b, const int32_t* seq_lens, const int32_t* qsl, int want,
+                                       long first_item) {
   std::vector<PrefillSplit> out(b.prefill.size());
-  if (sh->dtype == MPA_F32 || b.prefill.empty()) return out;
-  const int qt = q_tile(sh);
-  long units = 0;
-  for (int s : b.prefill) units += (long)(qsl[s + 1] - qsl[s] + qt - 1) / qt * sh->num_kv_heads;
-  if (units >= mpa::kPrefillSplitTarget) return out;
-  const int want = (int)((mpa::kPrefillSplitTarget + units - 1) / units);
   long item = first_item;
   for (size_t k = 0; k < b.prefill.size(); ++k) {
     const int s = b.prefill[k];
@@ -191,6 +227,95 @@ std::vector<PrefillSplit> prefill_splits(const mpa_shape* sh, const Batch& b, co
     item += (long)n * C;
   }
   return out;
+}
+
+// Predicted device time of the prefill launches for a split layout: per
+// launch (kMaxPrefillSeqs chunks), the makespan of its workgroups -- each
+// wg_us + tile_us per 64-key tile -- dealt in launch order (the longest
+// query tiles first) to `slots` slots that take the next workgroup when
+// free; plus, when a chunk of the launch is split, the merge: merge_us +
+// merge_row_us per partial (token, q head, split) row.
+double prefill_time(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens, const int32_t* qsl,
+                    const std::vector<PrefillSplit>& sp, double wg_us, double tile_us, int slots, double merge_us,
+                    double merge_row_us) {
+  const int qt = q_tile(sh);
+  double total = 0.0;
+  std::vector<int> tiles;
+  for (size_t c0 = 0; c0 < b.prefill.size(); c0 += mpa::kMaxPrefillSeqs) {
+    const size_t c1 = std::min(b.prefill.size(), c0 + mpa::kMaxPrefillSeqs);
+    tiles.clear();  // 64-key tiles of each work unit, in unit order
+    double partial_rows = 0.0;
+    for (size_t k = c0; k < c1; ++k) {
+      const int s = b.prefill[k];
+      const int C = qsl[s + 1] - qsl[s];
+      const int P = seq_lens[s] - C;
+      if (sp[k].nsplit > 1) partial_rows += (double)C * sh->num_q_heads * sp[k].nsplit;
+      for (int q = 0; q < (C + qt - 1) / qt; ++q) {
+        const int kend = P + std::min(q * qt + qt - 1, C - 1) + 1;
+        const int all = (kend + 63) / 64;
+        for (int x = 0; x < sp[k].nsplit; ++x)
+          tiles.push_back(x == sp[k].nsplit - 1 ? all - x * sp[k].tiles : sp[k].tiles);
+      }
+    }
+    std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
+    for (int i = 0; i < slots; ++i) free_at.push(0.0);
+    double makespan = 0.0;
+    // blockIdx order: the last unit first, each unit once per KV head
+    for (size_t u = tiles.size(); u-- > 0;)
+      for (int g = 0; g < sh->num_kv_heads; ++g) {
+        const double end = free_at.top() + wg_us + tile_us * tiles[u];
+        free_at.pop();
+        makespan = std::max(makespan, end);
+        free_at.push(end);
+      }
+    total += makespan + (partial_rows > 0 ? merge_us + merge_row_us * partial_rows : 0.0);
+  }
+  return total;
+}
+
+// The planner's own figures for prefill_time (those of mpa_default_rates),
+// fixed so that a batch always gets the same plan.
+constexpr double kPlanWgUs = 18.0;
+constexpr double kPlanTileUs = 1.85;
+constexpr double kPlanMergeUs = 3.0;
+constexpr double kPlanMergeRowUs = 1.6e-4;
+
+// The split count.  A batch with at least two workgroups per CU is not
+// split: its makespan is already close to its work over the CUs, and the
+// partial results would cost more than they balance.  A smaller batch gets
+// the split count (1, 2, ...) with the shortest predicted prefill time,
+// the fewer splits on a tie; counts past the point where every chunk's
+// prefix is cut as finely as allowed, or past 8 workgroups per CU, are not
+// tried.  MPA_PREFILL_SPLITS (1..64) overrides the choice for tuning sweeps.
+std::vector<PrefillSplit> prefill_splits(const mpa_shape* sh, const Batch& b, const int32_t* seq_lens,
+                                         const int32_t* qsl, long first_item) {
+  if (sh->dtype == MPA_F32 || b.prefill.empty()) return std::vector<PrefillSplit>(b.prefill.size());
+  if (const char* env = getenv("MPA_PREFILL_SPLITS")) {
+    const int v = atoi(env);
+    if (v >= 1 && v <= 64) return split_layout(b, seq_lens, qsl, v, first_item);
+  }
+  const int qt = q_tile(sh);
+  long units = 0;
+  int most = 1;  // the most splits any chunk can take
+  for (int s : b.prefill) {
+    const int C = qsl[s + 1] - qsl[s];
+    units += (long)(C + qt - 1) / qt * sh->num_kv_heads;
+    most = std::max(most, std::min(1 + (seq_lens[s] - C) / 64 / mpa::kPrefillMinSplitTiles, 64));
+  }
+  if (units >= 2L * mpa::kPrefillSplitTarget || most == 1) return std::vector<PrefillSplit>(b.prefill.size());
+  PlanMemo& m = plan_memo(sh, seq_lens, qsl);
+  if (m.want == 0) {
+    double best_t = -1.0;
+    for (int want = 1; want <= most && (want == 1 || units * want <= 8L * mpa::kPrefillSplitTarget); ++want) {
+      const double t = prefill_time(sh, b, seq_lens, qsl, split_layout(b, seq_lens, qsl, want, 0), kPlanWgUs,
+                                    kPlanTileUs, mpa::kPrefillSplitTarget, kPlanMergeUs, kPlanMergeRowUs);
+      if (best_t < 0 || t < best_t * (1.0 - 1e-9)) {
+        best_t = t;
+        m.want = want;
+      }
+    }
+  }
+  return split_layout(b, seq_lens, qsl, m.want, first_item);
 }
 
 long prefill_items(const std::vector<PrefillSplit>& sp, const Batch& b, const int32_t* qsl) {
@@ -337,7 +462,7 @@ mpa_step_time model_step(const mpa_shape* shape, const Batch& b, const int32_t* 
   }
 
   // decode, launch by launch as run_attention issues them
-  const int split = choose_split(shape, b, seq_lens_host);
+  const int split = choose_split(shape, b, seq_lens_host, qsl_host);
   const double head_bytes = 2.0 * shape->head_dim * elem;  // K + V of one token and KV head
   for (size_t c0 = 0; c0 < b.decode.size(); c0 += mpa::kMaxPlanSeqs) {
     const size_t c1 = std::min(b.decode.size(), c0 + mpa::kMaxPlanSeqs);
@@ -355,42 +480,12 @@ mpa_step_time model_step(const mpa_shape* shape, const Batch& b, const int32_t* 
 
   // prefill: each launch's workgroups, in launch order (longest query tiles
   // first), on prefill_slots slots that take the next workgroup when free
-  const int qt = q_tile(shape);
   const std::vector<PrefillSplit> psplit =
       prefill_splits(shape, b, seq_lens_host, qsl_host, decode_items(shape, b, seq_lens_host, split));
+  t.prefill_us = prefill_time(shape, b, seq_lens_host, qsl_host, psplit, r.prefill_wg_us, r.prefill_tile_us,
+                              r.prefill_slots, r.prefill_merge_us, r.prefill_merge_row_us);
   bool few = false;
-  for (size_t c0 = 0; c0 < b.prefill.size(); c0 += mpa::kMaxPrefillSeqs) {
-    const size_t c1 = std::min(b.prefill.size(), c0 + mpa::kMaxPrefillSeqs);
-    std::vector<int> tiles;  // 64-key tiles of each work unit, in unit order
-    bool launch_split = false;
-    for (size_t k = c0; k < c1; ++k) {
-      const int s = b.prefill[k];
-      const int C = qsl_host[s + 1] - qsl_host[s];
-      const int P = seq_lens_host[s] - C;
-      const PrefillSplit& ps = psplit[k];
-      launch_split |= ps.nsplit > 1;
-      few |= P < mpa::kFewKeys;
-      for (int q = 0; q < (C + qt - 1) / qt; ++q) {
-        const int kend = P + std::min(q * qt + qt - 1, C - 1) + 1;
-        const int all = (kend + 63) / 64;
-        for (int x = 0; x < ps.nsplit; ++x)
-          tiles.push_back(x == ps.nsplit - 1 ? all - x * ps.tiles : ps.tiles);
-      }
-    }
-    std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
-    for (int i = 0; i < r.prefill_slots; ++i) free_at.push(0.0);
-    double makespan = 0.0;
-    // blockIdx order: the last unit first, each unit once per KV head
-    for (size_t u = tiles.size(); u-- > 0;)
-      for (int g = 0; g < shape->num_kv_heads; ++g) {
-        const double start = free_at.top();
-        free_at.pop();
-        const double end = start + r.prefill_wg_us + r.prefill_tile_us * tiles[u];
-        makespan = std::max(makespan, end);
-        free_at.push(end);
-      }
-    t.prefill_us += makespan + (launch_split ? r.prefill_merge_us : 0.0);
-  }
+  for (int s : b.prefill) few |= seq_lens_host[s] - (qsl_host[s + 1] - qsl_host[s]) < mpa::kFewKeys;
   if (few) t.prefill_us += r.prefill_fixup_us;
   t.step_us = t.append_us + t.decode_us + t.prefill_us;
   return t;
@@ -416,7 +511,7 @@ const char* mpa_status_string(int status) {
     case MPA_OK: return "ok";
     case MPA_ERR_INVALID: return "invalid argument or batch metadata";
     case MPA_ERR_UNSUPPORTED: return "unsupported shape or dtype";
-    case MPA_ERR_WORKSPACE: return "workspace missing or too small";
+    case MPA_ERR_WORKSPACE: return "workspace missing, too small or not 16-byte aligned";
     case MPA_ERR_HIP: return "HIP launch error";
     default: return "unknown status";
   }
@@ -428,7 +523,7 @@ int mpa_get_plan_info(const mpa_shape* shape, const int32_t* seq_lens_host, cons
   Batch b;
   int rc = check_batch(shape, seq_lens_host, qsl_host, nullptr, false, &b);
   if (rc != MPA_OK) return rc;
-  const int split = choose_split(shape, b, seq_lens_host);
+  const int split = choose_split(shape, b, seq_lens_host, qsl_host);
   info->num_decode_seqs = (int32_t)b.decode.size();
   info->num_prefill_seqs = (int32_t)b.prefill.size();
   info->split_tokens = split;
@@ -468,7 +563,8 @@ void mpa_default_rates(mpa_rates* r) {
   r->merge_us = 5.0;
   r->prefill_wg_us = 18.0;
   r->prefill_tile_us = 1.85;
-  r->prefill_merge_us = 5.0;
+  r->prefill_merge_us = 3.0;
+  r->prefill_merge_row_us = 1.6e-4;
   r->prefill_fixup_us = 8.0;
   r->prefill_slots = 256;
   // CU-partitioned co-execution (mpa_plan_coexec), measured on agentic, lent
@@ -566,7 +662,7 @@ int mpa_partition_streams(int32_t mode, void** decode_stream, void** prefill_str
 size_t mpa_workspace_size(const mpa_shape* shape, const int32_t* seq_lens_host, const int32_t* qsl_host) {
   Batch b;
   if (check_batch(shape, seq_lens_host, qsl_host, nullptr, false, &b) != MPA_OK) return 0;
-  const int split = choose_split(shape, b, seq_lens_host);
+  const int split = choose_split(shape, b, seq_lens_host, qsl_host);
   bool any_split = false;
   for (int s : b.decode) any_split |= row_split(seq_lens_host[s], split).parts > 1;
   const long ditems = decode_items(shape, b, seq_lens_host, split);
@@ -629,7 +725,7 @@ int run_attention(int phases, const mpa_shape* shape, const void* q, const void*
   // the whole batch's, so the two halves can run concurrently.
   Batch all;
   check_batch(shape, seq_lens_host, query_start_loc_host, nullptr, false, &all);
-  const int split = choose_split(shape, all, seq_lens_host);
+  const int split = choose_split(shape, all, seq_lens_host, query_start_loc_host);
   const long ditems = decode_items(shape, all, seq_lens_host, split);
   const std::vector<PrefillSplit> psplit =
       prefill_splits(shape, all, seq_lens_host, query_start_loc_host, ditems);
@@ -640,7 +736,7 @@ int run_attention(int phases, const mpa_shape* shape, const void* q, const void*
     for (const auto& ps : psplit) any_split |= ps.nsplit > 1;
   if (any_split) {
     const size_t need = workspace_bytes(shape, items);
-    if (!workspace || workspace_bytes_given < need) return MPA_ERR_WORKSPACE;
+    if (!workspace || workspace_bytes_given < need || ((uintptr_t)workspace & 15) != 0) return MPA_ERR_WORKSPACE;
   }
   mpa::AttnArgs a;
   a.q = q;

@@ -489,53 +489,76 @@ __global__ __launch_bounds__(256) void decode_kernel(AttnArgs a, DecodePlan p) {
   }
 }
 
-// Split-K merge: one 64-lane workgroup per (decode sequence, query head).
-// With split maxima m_j and sums l_j (log2 units), the row's softmax
-// denominator is sum_j l_j 2^(m_j - M) with M = max_j m_j, and its output is
-// sum_j acc_j 2^(m_j - M) divided by that denominator.  Splits are taken 16
-// at a time with every load of a group issued before any is used, so a group
-// costs one memory latency.
-// One output row from n split-K partial results: m_k (row maximum, log2
-// units), l_k (sum of exp2(s - m_k)) and acc_k (sum of exp2(s - m_k) v) are
-// combined with the weights exp2(m_k - max m), 16 splits at a time with all
-// of a group's loads issued before any is used.  ml points at split 0's
-// (m, l) pair, acc at split 0's element `lane` of the row; consecutive splits
-// are ml_stride and acc_stride floats apart.  Lane l writes elements l,
-// l + 64, ... of out; lane 0 writes lse.
+// Split-K merge.  With split maxima m_k and sums l_k (log2 units), a row's
+// softmax denominator is sum_k l_k 2^(m_k - M) with M = max_k m_k, and its
+// output is sum_k acc_k 2^(m_k - M) divided by that denominator.
+//
+// One output row from n partial results, by one wave.  Splits are taken 64
+// at a time: lane k loads split k's (m, l) pair, the group's maximum and
+// weighted sum come from wave reductions, and the partial rows are then
+// loaded four at a time (all four issued before any is used), each weight
+// broadcast from its lane.  Only the n real splits are read.  ml points at
+// split 0's (m, l) pair (8-byte aligned), acc at split 0's element `lane` of
+// the row; consecutive splits are ml_stride and acc_stride floats apart.
+// Lane l writes elements l, l + 64, ... of out; lane 0 writes lse.
+__device__ inline float wave_max64(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x = fmaxf(x, __shfl_xor(x, off));
+  return x;
+}
+__device__ inline float wave_sum64(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+__device__ inline float lane_value(float x, int k) {  // k wave-uniform
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), k));
+}
+
 template <int DT, int D>
 __device__ inline void merge_splits(const float* ml, size_t ml_stride, const float* acc, size_t acc_stride, int n,
                                     typename Tr<DT>::QElem* out, float* lse) {
   using T = Tr<DT>;
   constexpr int PER = D / 64;
-  constexpr int GRP = 16;
+  constexpr int U = 4;
   const int lane = threadIdx.x & 63;
   float M = -INFINITY, lsum = 0.f;
   float o[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) o[e] = 0.f;
-  for (int c0 = 0; c0 < n; c0 += GRP) {
-    float mj[GRP], lj[GRP], vj[GRP][PER];
-#pragma unroll
-    for (int k = 0; k < GRP; ++k) {
-      const int i = min(c0 + k, n - 1);  // past the end: a repeat, weighted 0 below
-      mj[k] = ml[(size_t)i * ml_stride];
-      lj[k] = ml[(size_t)i * ml_stride + 1];
-#pragma unroll
-      for (int e = 0; e < PER; ++e) vj[k][e] = acc[(size_t)i * acc_stride + 64 * e];
+  for (int c0 = 0; c0 < n; c0 += 64) {
+    const int cnt = min(64, n - c0);
+    float mk = -INFINITY, lk = 0.f;
+    if (lane < cnt) {
+      const float2 v = *reinterpret_cast<const float2*>(ml + (size_t)(c0 + lane) * ml_stride);
+      mk = v.x;
+      lk = v.y;
     }
-    float gm = M;
-#pragma unroll
-    for (int k = 0; k < GRP; ++k) gm = fmaxf(gm, mj[k]);
-    const float rescale = exp2_fast(M - gm);  // M = -inf on the first group: 0
-    lsum *= rescale;
+    const float gm = fmaxf(M, wave_max64(mk));      // every split holds a key: finite
+    const float wk = lane < cnt ? exp2_fast(mk - gm) : 0.f;
+    const float rescale = exp2_fast(M - gm);        // M = -inf on the first group: 0
+    lsum = lsum * rescale + wave_sum64(wk * lk);
 #pragma unroll
     for (int e = 0; e < PER; ++e) o[e] *= rescale;
+    const float* a0 = acc + (size_t)c0 * acc_stride;
+    int k = 0;
+    for (; k + U <= cnt; k += U) {
+      float v[U][PER];
 #pragma unroll
-    for (int k = 0; k < GRP; ++k) {
-      const float w = c0 + k < n ? exp2_fast(mj[k] - gm) : 0.f;
-      lsum += w * lj[k];
+      for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int e = 0; e < PER; ++e) o[e] += w * vj[k][e];
+        for (int e = 0; e < PER; ++e) v[u][e] = a0[(size_t)(k + u) * acc_stride + 64 * e];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const float w = lane_value(wk, k + u);
+#pragma unroll
+        for (int e = 0; e < PER; ++e) o[e] += w * v[u][e];
+      }
+    }
+    for (; k < cnt; ++k) {
+      const float w = lane_value(wk, k);
+#pragma unroll
+      for (int e = 0; e < PER; ++e) o[e] += w * a0[(size_t)k * acc_stride + 64 * e];
     }
     M = gm;
   }
@@ -545,31 +568,40 @@ __device__ inline void merge_splits(const float* ml, size_t ml_stride, const flo
   if (lse && lane == 0) *lse = (M + log2f(lsum)) * kLn2;
 }
 
-// Decode merge: one 64-lane workgroup per (split decode sequence, q head).
+// The merge kernels run four waves per workgroup, each wave merging whole
+// (row, q head) pairs on its own (no LDS, no barrier): a launch with one
+// small workgroup per pair is bound by the dispatcher's workgroup rate
+// (about 1.2 per ns), not by the bytes it moves.
+constexpr int kMergeWaves = 4;
+constexpr int kPrefillMergeHeadsPerWave = 4;
+
+// Decode merge: one workgroup per (split decode sequence, 4 q heads); wave w
+// merges head 4 * blockIdx.y + w.
 template <int DT, int D>
-__global__ __launch_bounds__(64) void merge_kernel(AttnArgs a, DecodePlan p) {
+__global__ __launch_bounds__(64 * kMergeWaves) void merge_kernel(AttnArgs a, DecodePlan p) {
   using E = typename Tr<DT>::QElem;
   const int j = blockIdx.x;
-  const int h = blockIdx.y;
-  if (j >= p.n_seqs) return;
+  const int h = blockIdx.y * kMergeWaves + wave_uniform(threadIdx.x >> 6);
+  if (j >= p.n_seqs || h >= a.hq) return;
   const int n = p.item_start[j + 1] - p.item_start[j];
   if (n <= 1) return;
   const int s = p.seq[j];
   const size_t base = (size_t)p.item_base + p.item_start[j];
   const int t = a.qsl[s];
+  const int lane = threadIdx.x & 63;
   merge_splits<DT, D>(a.ws_ml + (base * a.hq + h) * 2, (size_t)a.hq * 2,
-                      a.ws_o + (base * a.hq + h) * D + threadIdx.x, (size_t)a.hq * D, n,
+                      a.ws_o + (base * a.hq + h) * D + lane, (size_t)a.hq * D, n,
                       reinterpret_cast<E*>(a.out) + ((size_t)t * a.hq + h) * D,
                       a.lse ? a.lse + (size_t)t * a.hq + h : nullptr);
 }
 
-// Prefill merge: one 64-lane workgroup per (token of a KV-split chunk, q
-// head); split x of token i of chunk j sits at slot item_base[j] + x*C + i.
+// Prefill merge: one workgroup per (token of a KV-split chunk, 16 q heads);
+// wave w merges heads 16 * blockIdx.y + w + 4 * k, k < 4.  Split x of token
+// i of chunk j sits at slot item_base[j] + x*C + i.
 template <int DT, int D>
-__global__ __launch_bounds__(64) void prefill_merge_kernel(AttnArgs a, PrefillPlan p) {
+__global__ __launch_bounds__(64 * kMergeWaves) void prefill_merge_kernel(AttnArgs a, PrefillPlan p) {
   using E = typename Tr<DT>::QElem;
   const int r = blockIdx.x;
-  const int h = blockIdx.y;
   if (r >= p.row_start[p.n_seqs]) return;
   const int j = upper_index(p.row_start, p.n_seqs, r);
   const int s = p.seq[j];
@@ -577,10 +609,16 @@ __global__ __launch_bounds__(64) void prefill_merge_kernel(AttnArgs a, PrefillPl
   const int t0 = a.qsl[s];
   const int C = a.qsl[s + 1] - t0;
   const size_t slot = (size_t)p.item_base[j] + i;
-  merge_splits<DT, D>(a.ws_ml + (slot * a.hq + h) * 2, (size_t)C * a.hq * 2,
-                      a.ws_o + (slot * a.hq + h) * D + threadIdx.x, (size_t)C * a.hq * D, p.nsplit[j],
-                      reinterpret_cast<E*>(a.out) + ((size_t)(t0 + i) * a.hq + h) * D,
-                      a.lse ? a.lse + (size_t)(t0 + i) * a.hq + h : nullptr);
+  const int lane = threadIdx.x & 63;
+  const int h0 = blockIdx.y * (kMergeWaves * kPrefillMergeHeadsPerWave) + wave_uniform(threadIdx.x >> 6);
+  for (int k = 0; k < kPrefillMergeHeadsPerWave; ++k) {
+    const int h = h0 + k * kMergeWaves;
+    if (h >= a.hq) break;
+    merge_splits<DT, D>(a.ws_ml + (slot * a.hq + h) * 2, (size_t)C * a.hq * 2,
+                        a.ws_o + (slot * a.hq + h) * D + lane, (size_t)C * a.hq * D, p.nsplit[j],
+                        reinterpret_cast<E*>(a.out) + ((size_t)(t0 + i) * a.hq + h) * D,
+                        a.lse ? a.lse + (size_t)(t0 + i) * a.hq + h : nullptr);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1346,7 +1384,8 @@ template <int DT, int D>
 struct MergeL {
   static hipError_t run(const AttnArgs& a, const DecodePlan& p, hipStream_t stream) {
     if (p.n_seqs == 0) return hipSuccess;
-    hipLaunchKernelGGL((merge_kernel<DT, D>), dim3(p.n_seqs, a.hq), dim3(64), 0, stream, a, p);
+    hipLaunchKernelGGL((merge_kernel<DT, D>), dim3(p.n_seqs, (a.hq + kMergeWaves - 1) / kMergeWaves),
+                       dim3(64 * kMergeWaves), 0, stream, a, p);
     return hipGetLastError();
   }
 };
@@ -1452,7 +1491,9 @@ struct PrefillMergeL {
   static hipError_t run(const AttnArgs& a, const PrefillPlan& p, hipStream_t stream) {
     const int rows = p.row_start[p.n_seqs];
     if (rows == 0) return hipSuccess;
-    hipLaunchKernelGGL((prefill_merge_kernel<DT, D>), dim3(rows, a.hq), dim3(64), 0, stream, a, p);
+    constexpr int heads = kMergeWaves * kPrefillMergeHeadsPerWave;
+    hipLaunchKernelGGL((prefill_merge_kernel<DT, D>), dim3(rows, (a.hq + heads - 1) / heads),
+                       dim3(64 * kMergeWaves), 0, stream, a, p);
     return hipGetLastError();
   }
 };

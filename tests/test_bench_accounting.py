@@ -1,8 +1,11 @@
 """The benchmark's algorithmic byte / FLOP accounting on a hand-sized batch,
-and its refusal of more than one GPU (CPU only)."""
+its refusal of more than one GPU, and the tensor-parallel workload share
+(CPU only)."""
 
 import subprocess
 import sys
+
+import pytest
 
 import bench
 
@@ -25,3 +28,20 @@ def test_algorithmic_work_hand_example():
 def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, bench.__file__, "--gpus", "2"], capture_output=True, text=True)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_tensor_parallel_share_keeps_the_sequences():
+    """One GPU's share of a TP layout: the same sequences (same draws) with
+    1/tp of both head counts; head counts that do not divide are refused."""
+    from workloads.configs import config_specs
+
+    for name in ("decode8b", "agentic", "longctx"):
+        s1, h1, nb1, _ = config_specs(name, 3)
+        s4, h4, nb4, _ = config_specs(name, 3, tp=4)
+        assert s1 == s4 and nb1 == nb4
+        assert (h4.num_q_heads * 4, h4.num_kv_heads * 4) == (h1.num_q_heads, h1.num_kv_heads)
+        assert (h4.head_dim, h4.block_size) == (h1.head_dim, h1.block_size)
+    with pytest.raises(ValueError):
+        config_specs("decode8b", 0, tp=16)  # 8 KV heads
+    with pytest.raises(ValueError):
+        config_specs("tiny", 0, tp=4)  # 2 KV heads

@@ -243,9 +243,10 @@ def test_decode_split_boundaries(torch_gpu, dtype, monkeypatch):
     """Decode rows whose lengths sit at and around multiples of a forced
     128-token nominal split: every row is cut into ceil(L / 128) equal parts
     rounded up to whole blocks, so part edges fall inside blocks of the
-    nominal grid and the last part is short or full."""
+    nominal grid and the last part is short or full.  Rows of 64, 65 and 129
+    parts cross the merge's groups of 64 splits."""
     monkeypatch.setenv("MPA_SPLIT_TOKENS", "128")
-    lens = [1, 15, 16, 17, 127, 128, 129, 143, 144, 255, 256, 257, 383, 1000, 1025, 4097]
+    lens = [1, 15, 16, 17, 127, 128, 129, 143, 144, 255, 256, 257, 383, 1000, 1025, 4097, 8192, 8193, 16400]
     b = make_batch([SeqSpec(L, 1) for L in lens], HeadSpec(16, 4, 128), dtype, np.random.default_rng(70))
     sh = mpa.make_shape(num_seqs=b.num_seqs, num_q_heads=16, num_kv_heads=4, head_dim=128, num_blocks=b.num_blocks,
                         max_blocks_per_seq=b.block_tables.shape[1], total_q_tokens=b.total_q, scale=b.scale,
@@ -515,14 +516,21 @@ def oracle_rows(b, s, rows):
 FULL = ["decode8b", "lent", "agentic", "budget0", "budget256", "budget1024", "budget4096", "longctx"]
 
 
-@pytest.mark.parametrize("name,dtype", [(n, "bf16") for n in FULL] + [("decode8b", "fp8"), ("lent", "fp8")],
-                         ids=lambda x: x if isinstance(x, str) else None)
-def test_full_size_sampled(torch_gpu, name, dtype):
+# one GPU's share of the paper's TP4 decode workers: 8/2 heads (G = 4), and
+# 16/2 (G = 8) for agentic
+FULL_TP4 = ["decode8b", "agentic", "budget256", "longctx"]
+
+
+@pytest.mark.parametrize("name,dtype,tp", [(n, "bf16", 1) for n in FULL] + [("decode8b", "fp8", 1), ("lent", "fp8", 1)]
+                         + [(n, "bf16", 4) for n in FULL_TP4],
+                         ids=lambda x: x if isinstance(x, str) else f"tp{x}")
+def test_full_size_sampled(torch_gpu, name, dtype, tp):
     import torch
 
     seed = 0
-    specs, heads, nb, rng = config_specs(name, seed)
-    say(f"[gpu] full size {name} {dtype}: {len(specs)} seqs, T={sum(s.q_len for s in specs)}")
+    specs, heads, nb, rng = config_specs(name, seed, tp=tp)
+    say(f"[gpu] full size {name} {dtype} tp{tp}: {len(specs)} seqs, T={sum(s.q_len for s in specs)}, "
+        f"{heads.num_q_heads}/{heads.num_kv_heads} heads")
     d = device_step(specs, heads, dtype, rng, seed, num_blocks=nb)
     srng = np.random.default_rng(1000 + seed)
     dec = [i for i, s in enumerate(specs) if s.q_len == 1]

@@ -19,7 +19,7 @@ FAKE = 0x1000  # a non-null pointer value; never dereferenced because validation
 def declared_functions():
     src = open(HEADER).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(mpa_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(mpa_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_library_exports_every_declared_symbol():
@@ -34,7 +34,7 @@ def declared_arity():
     """Parameter count of every function include/mpa.h declares."""
     src = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
     out = {}
-    for name, params in re.findall(r"\b(mpa_[a-z_]+)\s*\(([^;{]*?)\)\s*;", src, flags=re.S):
+    for name, params in re.findall(r"\b(mpa_[a-z0-9_]+)\s*\(([^;{]*?)\)\s*;", src, flags=re.S):
         params = params.strip()
         out[name] = 0 if params in ("", "void") else params.count(",") + 1
     return out
@@ -63,14 +63,14 @@ def shape(**kw):
     return mpa.make_shape(**base)
 
 
-def attention_rc(sh, seq_lens, qsl, bt=None, ws=0):
+def attention_rc(sh, seq_lens, qsl, bt=None, ws=0, ws_ptr=None):
     L = mpa.lib()
     sl = np.asarray(seq_lens, np.int32)
     qs = np.asarray(qsl, np.int32)
     bth = None if bt is None else np.asarray(bt, np.int32)
     return L.mpa_mixed_paged_attention(
         ctypes.byref(sh), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, mpa._i32p(sl), mpa._i32p(qs), mpa._i32p(bth), FAKE,
-        None, None, ws, None)
+        None, ws_ptr, ws, None)
 
 
 def append_rc(sh, seq_lens, qsl, bt=None):
@@ -154,6 +154,10 @@ def test_workspace_required_for_split_rows():
     assert items == -(-9000 // info.split_tokens)
     assert n == items * 8 * (128 + 2) * 4
     assert attention_rc(sh, seq_lens, qsl, ws=n - 1) == mpa.MPA_ERR_WORKSPACE
+    # the partials' (max, sum) pairs are read as 8-byte vectors: a workspace
+    # that is not 16-byte aligned is refused before any launch
+    for off in (4, 8):
+        assert attention_rc(sh, seq_lens, qsl, ws=n + 64, ws_ptr=FAKE + off) == mpa.MPA_ERR_WORKSPACE
 
 
 def test_no_workspace_for_short_rows():
@@ -254,3 +258,51 @@ def test_debug_append_slot_checks(monkeypatch):
     own = bt.copy()
     own[1, 2] = own[1, 0]
     assert append_rc(sh, sl, qsl, own) == mpa.MPA_ERR_INVALID
+
+
+def test_probe_arguments_rejected_before_launch():
+    L = mpa.lib()
+    sink = ctypes.c_void_p(FAKE)
+    for buf, n in ((None, 16), (FAKE, 0), (FAKE, 24), (FAKE + 8, 32)):
+        assert L.mpa_probe_stream_read(buf, n, sink, None) == mpa.MPA_ERR_INVALID
+    assert L.mpa_probe_stream_read(FAKE, 16, None, None) == mpa.MPA_ERR_INVALID
+    for iters in (0, -5):
+        assert L.mpa_probe_mfma_bf16(iters, sink, None, None) == mpa.MPA_ERR_INVALID
+    assert L.mpa_probe_mfma_bf16(10, None, None, None) == mpa.MPA_ERR_INVALID
+
+
+def test_plan_memo_matches_fresh_planning(monkeypatch):
+    """The per-thread memo of the split choices: planning batches A, B, A in
+    turn gives what a fresh thread (empty memo) gives for each, a batch that
+    differs in one length is planned anew, and the tuning overrides are part
+    of the key."""
+    import threading
+
+    def batch(last):
+        sl = [9000, 5000, 700, 4352 + 256, 2048 + last]
+        qsl = [0, 1, 2, 3, 3 + 256, 3 + 256 + last]
+        sh = mpa.make_shape(num_seqs=5, num_q_heads=8, num_kv_heads=2, head_dim=128, num_blocks=2000,
+                            max_blocks_per_seq=1024, total_q_tokens=qsl[-1], scale=128 ** -0.5, dtype=mpa.MPA_BF16)
+        return sh, np.asarray(sl, np.int32), np.asarray(qsl, np.int32)
+
+    def plan(args):
+        i = mpa.plan_info(*args)
+        return (i.split_tokens, i.num_decode_items, i.prefill_max_splits, mpa.workspace_size(*args))
+
+    def fresh(args):
+        out = []
+        t = threading.Thread(target=lambda: out.append(plan(args)))
+        t.start()
+        t.join()
+        return out[0]
+
+    a, b = batch(512), batch(640)
+    pa, pb = plan(a), plan(b)
+    assert plan(a) == pa == fresh(a) and pb == fresh(b)
+    monkeypatch.setenv("MPA_SPLIT_TOKENS", "256")
+    monkeypatch.setenv("MPA_PREFILL_SPLITS", "3")
+    forced = plan(a)
+    assert forced[0] == 256 and forced[2] == 3 and forced == fresh(a)
+    monkeypatch.delenv("MPA_SPLIT_TOKENS")
+    monkeypatch.delenv("MPA_PREFILL_SPLITS")
+    assert plan(a) == pa

@@ -45,6 +45,7 @@ def unit_rates(**over):
               "prefill_fixup_us"):
         setattr(r, k, 0.0)
     r.append_block_us = 0.0
+    r.prefill_merge_row_us = 0.0
     r.append_gbs = r.append_block_gbs = r.decode_gbs = r.decode_wave_gbs = 1e12  # bandwidth terms ~0
     r.prefill_tile_us = 1.0
     for k, v in over.items():

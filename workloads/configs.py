@@ -27,6 +27,7 @@ per-step prefill token budget as the lease's compute credit (section 4.2).
 
 from __future__ import annotations
 
+import dataclasses
 import math
 
 import numpy as np
@@ -100,11 +101,21 @@ CONFIGS = {
 }
 
 
-def config_specs(name: str, seed: int):
+def config_specs(name: str, seed: int, tp: int = 1):
     """Draw a config's sequence list; returns (specs, heads, num_blocks, rng),
-    the rng positioned for the block permutation and the values."""
+    the rng positioned for the block permutation and the values.
+
+    ``tp`` > 1 gives one GPU's share of a tp-way tensor-parallel layout: the
+    same sequences with num_q_heads / tp query heads and num_kv_heads / tp KV
+    heads (the paper's decode workers run TP4, section 6.1).  Both head counts
+    must divide by tp."""
     rng = np.random.default_rng(seed)
     specs, heads, nb = CONFIGS[name](rng)
+    if tp != 1:
+        if tp < 1 or heads.num_q_heads % tp or heads.num_kv_heads % tp:
+            raise ValueError(f"{name}: {heads.num_q_heads} q / {heads.num_kv_heads} kv heads do not split {tp} ways")
+        heads = dataclasses.replace(heads, num_q_heads=heads.num_q_heads // tp,
+                                    num_kv_heads=heads.num_kv_heads // tp)
     return specs, heads, nb, rng
 
 
