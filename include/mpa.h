@@ -314,6 +314,7 @@ typedef struct {
   double coexec_prefill_q3;  /* ... on 3/4 */
   double coexec_slowdown;    /* two halves side by side over the slower one alone (>= 1) */
   double prefill_merge_row_us; /* KV-split merge, per partial (token, q head, split) row */
+  double coexec_fixed_us;      /* fixed cost of a step run on partitioned streams (>= 0) */
 } mpa_rates;
 
 typedef struct {
@@ -342,9 +343,12 @@ int mpa_predict_step(const mpa_shape* shape, const int32_t* seq_lens_host,
  * the prefill half on the rest (mpa_partition_streams).  The outputs are
  * bit-identical in every mode.  The predicted attention time of mode k is
  *   mode 0: decode + prefill of mpa_predict_step
- *   mode k: max(decode / coexec_decode_qk, prefill / coexec_prefill_q(4-k))
- *           * coexec_slowdown
- * (infinite when the step lacks decode rows or prefill chunks).
+ *   mode k: max(decode / coexec_decode_qk, prefill_k) * coexec_slowdown
+ *           + coexec_fixed_us
+ * with prefill_k = prefill * max(1, rounds_k * s / coexec_prefill_q(4-k)),
+ * s = (4 - k) / 4 the prefill half's share of the CUs and rounds_k the
+ * makespan of the prefill workgroups on s * prefill_slots slots over that on
+ * all of them (infinite when the step lacks decode rows or prefill chunks).
  *
  * mode          out: the mode with the shortest predicted time
  * predicted_us  out, may be NULL: double[4], the prediction per mode

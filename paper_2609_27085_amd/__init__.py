@@ -113,6 +113,7 @@ class MpaRates(ctypes.Structure):
         ("coexec_prefill_q3", ctypes.c_double),
         ("coexec_slowdown", ctypes.c_double),
         ("prefill_merge_row_us", ctypes.c_double),
+        ("coexec_fixed_us", ctypes.c_double),
     ]
 
 

@@ -565,6 +565,13 @@ void mpa_default_rates(mpa_rates* r) {
   r->prefill_tile_us = 1.85;
   r->prefill_merge_us = 3.0;
   r->prefill_merge_row_us = 1.6e-4;
+  // A partitioned step's fixed cost beyond the model (the cross-stream waits,
+  // and interference that the slowdown factor underrates on short steps):
+  // fitted with coexec_slowdown to the five partitioned steps measured
+  // against one stream (agentic and budget4096 at 64/8 and 32/8 heads, and
+  // lent and budget4096 at a quarter of the heads, where partitioning lost
+  // 14-16 %)
+  r->coexec_fixed_us = 80.0;
   r->prefill_fixup_us = 8.0;
   r->prefill_slots = 256;
   // CU-partitioned co-execution (mpa_plan_coexec), measured on agentic, lent
@@ -611,13 +618,31 @@ int mpa_plan_coexec(const mpa_shape* shape, const int32_t* seq_lens_host, const 
   if (!(r.coexec_slowdown >= 1.0)) return MPA_ERR_INVALID;
   for (int k = 1; k <= 3; ++k)
     if (!(dfrac[k] > 0) || !(pfrac[k] > 0)) return MPA_ERR_INVALID;
+  if (!(r.coexec_fixed_us >= 0.0)) return MPA_ERR_INVALID;
   const mpa_step_time serial = model_step(shape, b, seq_lens_host, qsl_host, r);
   double t[4];
   t[0] = serial.decode_us + serial.prefill_us;
-  for (int k = 1; k <= 3; ++k)
-    t[k] = b.decode.empty() || b.prefill.empty()
-               ? INFINITY  // nothing to overlap
-               : std::max(serial.decode_us / dfrac[k], serial.prefill_us / pfrac[k]) * r.coexec_slowdown;
+  // The prefill half on the (4 - k) / 4 of the CUs: its workgroups' makespan
+  // on that share of the slots relative to all of them (more rounds when the
+  // batch has few workgroups), times the per-CU speed measured on that share
+  // (pfrac against the share itself), and never faster than alone on the
+  // whole device.
+  const std::vector<PrefillSplit> ps = prefill_splits(shape, b, seq_lens_host, qsl_host, 0);
+  const double all_slots = prefill_time(shape, b, seq_lens_host, qsl_host, ps, r.prefill_wg_us, r.prefill_tile_us,
+                                        r.prefill_slots, 0.0, 0.0);
+  for (int k = 1; k <= 3; ++k) {
+    if (b.decode.empty() || b.prefill.empty()) {
+      t[k] = INFINITY;  // nothing to overlap
+      continue;
+    }
+    const double share = (4 - k) / 4.0;
+    const int slots = std::max(1, (int)lround(r.prefill_slots * share));
+    const double rounds = prefill_time(shape, b, seq_lens_host, qsl_host, ps, r.prefill_wg_us, r.prefill_tile_us,
+                                       slots, 0.0, 0.0) /
+                          all_slots;
+    const double prefill_k = serial.prefill_us * std::max(1.0, rounds * share / pfrac[k]);
+    t[k] = std::max(serial.decode_us / dfrac[k], prefill_k) * r.coexec_slowdown + r.coexec_fixed_us;
+  }
   int best = 0;
   for (int k = 1; k <= 3; ++k)
     if (t[k] < t[best]) best = k;
