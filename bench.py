@@ -250,6 +250,10 @@ def main(argv=None) -> int:
     ap.add_argument("--tp", type=int, default=1, choices=(1, 2, 4, 8),
                     help="run one GPU's share of a tp-way tensor-parallel layout: the same sequences with "
                          "1/tp of the query and KV heads (the paper's decode workers run TP4)")
+    ap.add_argument("--flush-mb", type=int, default=0, metavar="MB",
+                    help="read MB megabytes of device memory before every timed step (cache flush) and time each "
+                         "step with events; value then comes from the median step (default 0: back-to-back steps, "
+                         "wall clock)")
     ap.add_argument("--graph", action="store_true",
                     help="also capture one step into a HIP graph (torch.cuda.graph) and time its replays")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -363,16 +367,35 @@ def main(argv=None) -> int:
     dom = "decode" if has_dec and (not has_pre or phase_ms["decode"] >= phase_ms["prefill"]) else "prefill"
     dom_marks = list(spans[dom])
 
-    events = [new_events(dom_marks) for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(args.steps):
-        step(events[k])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+    if args.flush_mb:
+        # a streaming read of flush_mb MB before every timed step, which
+        # evicts the step's data from L2 and the MALL without leaving dirty
+        # lines (a write flush would leave its own write-back to drain into
+        # the step), each step timed on its own with events from start to
+        # end: value from the median step
+        flush = torch.zeros(args.flush_mb << 20, dtype=torch.uint8, device="cuda")
+        sink = torch.zeros(4, dtype=torch.uint8, device="cuda")
+        mpa.probe_stream_read(flush, sink)
+        events = [new_events(sorted(set(dom_marks) | {"start", "end"})) for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        for k in range(args.steps):
+            mpa.probe_stream_read(flush, sink)
+            step(events[k])
+        torch.cuda.synchronize()
+        ms_per_step = float(np.median([e["start"].elapsed_time(e["end"]) for e in events]))
+        value = work["query_tokens"] / (ms_per_step * 1e-3)
+        del flush
+    else:
+        events = [new_events(dom_marks) for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in range(args.steps):
+            step(events[k])
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ms_per_step = wall * 1e3 / args.steps
+        value = work["query_tokens"] * args.steps / wall
     dom_ms = avg_ms(events, dom)
-    ms_per_step = wall * 1e3 / args.steps
-    value = work["query_tokens"] * args.steps / wall
     # the dominant phase from the timed steps, the other from the calibration pass
     timed = dict(phase_ms)
     timed[dom] = dom_ms
@@ -414,6 +437,8 @@ def main(argv=None) -> int:
                                + (f"; one GPU's share of TP{args.tp}: {heads.num_q_heads}/{heads.num_kv_heads} heads"
                                   if args.tp > 1 else ""),
                    "seed": args.seed, "streams": args.streams if two else 1,
+                   "timing": (f"median of per-step events, {args.flush_mb} MB device read before each step"
+                              if args.flush_mb else "wall clock over back-to-back steps"),
                    "kv_cache": "bf16" if args.kv == "bf16" else "fp8 e4m3 (per-cache scale)",
                    "decode_rows": work["decode_rows"], "prefill_chunks": work["prefill_chunks"],
                    "query_tokens": work["query_tokens"],
