@@ -1,9 +1,12 @@
 #!/usr/bin/env python3
 """Throughput of one mixed prefill+decode attention step on one MI355X.
 
-A step is the whole hot path on one batch: mpa_kv_append, then the decode
-rows (split-K + merge) and the prefill chunks (causal MFMA tiles), all
-through the C ABI on one stream.  Inputs are synthetic and resident in HBM
+A step is the whole hot path on one batch: the append of the step's new K/V
+rows, the decode rows (split-K + merge) and the prefill chunks (causal MFMA
+tiles), all through the C ABI on one stream.  By default the append runs
+inside the attention calls (mpa_append_prefill_attention, then
+mpa_append_decode_attention, whose decode kernel writes the decode rows' new
+tokens); --append separate calls mpa_kv_append first.  Inputs are synthetic and resident in HBM
 before timing starts.  Prints one JSON line:
 
   value          query tokens/s over the timed steps (T * steps / wall time)
@@ -250,6 +253,10 @@ def main(argv=None) -> int:
     ap.add_argument("--tp", type=int, default=1, choices=(1, 2, 4, 8),
                     help="run one GPU's share of a tp-way tensor-parallel layout: the same sequences with "
                          "1/tp of the query and KV heads (the paper's decode workers run TP4)")
+    ap.add_argument("--append", default="fused", choices=("fused", "separate"),
+                    help="fused (default): the append inside the attention calls (mpa_append_prefill_attention, "
+                         "mpa_append_decode_attention: the decode kernel writes the decode rows' new tokens); "
+                         "separate: mpa_kv_append, then the attention")
     ap.add_argument("--flush-mb", type=int, default=0, metavar="MB",
                     help="read MB megabytes of device memory before every timed step (cache flush) and time each "
                          "step with events; value then comes from the median step (default 0: back-to-back steps, "
@@ -287,6 +294,11 @@ def main(argv=None) -> int:
     d = device_step(specs, heads, args.kv, rng, args.seed, num_blocks=nb)
     work = algorithmic_work(d.seq_lens_host, d.qsl_host, heads.num_q_heads, heads.num_kv_heads, heads.head_dim, 2,
                             kv_bytes=1 if args.kv == "fp8" else 2)
+    fused = args.append == "fused"
+    if fused:  # the decode rows' new K/V are read and written inside the decode phase
+        moved = 2 * work["decode_rows"] * heads.num_kv_heads * heads.head_dim * (2 + (1 if args.kv == "fp8" else 2))
+        work["decode_bytes"] += moved
+        work["append_bytes"] -= moved
     sc = dict(k_scale=d.k_scale, v_scale=d.v_scale)
     ws = mpa.alloc_workspace(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.qsl_host, d.scale)
     out = torch.empty_like(d.q)
@@ -316,8 +328,9 @@ def main(argv=None) -> int:
                 ev[name].record(s)
 
         mark("start", stream)
-        mpa.kv_append(d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
-                      d.seq_lens_host, d.qsl_host, stream=stream, **sc)
+        if not fused:
+            mpa.kv_append(d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
+                          d.seq_lens_host, d.qsl_host, stream=stream, **sc)
         mark("append", stream)
         pre_stream = dec_stream = stream
         if two:
@@ -328,14 +341,24 @@ def main(argv=None) -> int:
             dec_stream.wait_stream(stream)
             pre_stream.wait_stream(stream)
         if has_pre:
-            mpa.prefill_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
-                                  d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws, scale=d.scale,
-                                  stream=pre_stream, **sc)
+            if fused:
+                mpa.append_attention(d.q, d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens,
+                                     d.query_start_loc, d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws,
+                                     scale=d.scale, stream=pre_stream, which="mpa_append_prefill_attention", **sc)
+            else:
+                mpa.prefill_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
+                                      d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws, scale=d.scale,
+                                      stream=pre_stream, **sc)
         mark("prefill", pre_stream)
         if has_dec:
-            mpa.decode_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
-                                 d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws, scale=d.scale,
-                                 stream=dec_stream, **sc)
+            if fused:
+                mpa.append_attention(d.q, d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens,
+                                     d.query_start_loc, d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws,
+                                     scale=d.scale, stream=dec_stream, which="mpa_append_decode_attention", **sc)
+            else:
+                mpa.decode_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
+                                     d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws, scale=d.scale,
+                                     stream=dec_stream, **sc)
         mark("decode", dec_stream)
         if two:
             stream.wait_stream(side)
@@ -437,6 +460,8 @@ def main(argv=None) -> int:
                                + (f"; one GPU's share of TP{args.tp}: {heads.num_q_heads}/{heads.num_kv_heads} heads"
                                   if args.tp > 1 else ""),
                    "seed": args.seed, "streams": args.streams if two else 1,
+                   "append": ("fused into the attention halves (decode rows by the decode kernel)" if fused
+                              else "mpa_kv_append before the attention"),
                    "timing": (f"median of per-step events, {args.flush_mb} MB device read before each step"
                               if args.flush_mb else "wall clock over back-to-back steps"),
                    "kv_cache": "bf16" if args.kv == "bf16" else "fp8 e4m3 (per-cache scale)",

@@ -215,6 +215,52 @@ int mpa_mixed_paged_attention(const mpa_shape* shape, const void* q, const void*
                               void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * One whole step of the mixed iteration in one call: mpa_kv_append followed
+ * by mpa_mixed_paged_attention on the same batch, with results (cache
+ * contents, out, lse) bit-identical to the two calls.  The decode rows
+ * extend the KV cache by one token each (section 2.1) and the chunk's KV is
+ * materialised on the reused prefix before it is attended to (section 4.4);
+ * here a decode row's new token is written by the decode kernel itself --
+ * by the wave that reads the row's last split, the only one whose keys
+ * include it -- which saves the per-token append launch, while multi-token
+ * rows keep their own append launch ahead of the prefill kernel.
+ *
+ * k_new, v_new      device [T][Hkv][d] (bf16 for fp8 caches), as for
+ *                   mpa_kv_append; may be NULL only when T == 0
+ * k_cache, v_cache  written (the new tokens) and read
+ * Other arguments as for mpa_mixed_paged_attention.  Every check of both
+ * calls (the workspace included) runs before the first launch: an error
+ * return means nothing was launched.  With MPA_DEBUG=1 the append's slot
+ * checks apply.
+ */
+int mpa_append_attention(const mpa_shape* shape, const void* q, const void* k_new, const void* v_new,
+                         void* k_cache, void* v_cache, const int32_t* block_tables, const int32_t* seq_lens,
+                         const int32_t* query_start_loc, const int32_t* seq_lens_host,
+                         const int32_t* query_start_loc_host, const int32_t* block_tables_host, void* out,
+                         float* lse, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The two halves of mpa_append_attention, as mpa_decode_attention and
+ * mpa_prefill_attention are of mpa_mixed_paged_attention: the decode half
+ * appends and attends the rows of sequences with q_len == 1 (the decode
+ * kernel writing their new tokens), the prefill half appends the new tokens
+ * of sequences with q_len > 1 (by cache block) and then attends their rows.
+ * Same arguments and checks as mpa_append_attention; running both gives its
+ * results bit for bit.  The halves write disjoint cache slots, rows and
+ * workspace, read none of each other's new keys, and may run concurrently.
+ */
+int mpa_append_decode_attention(const mpa_shape* shape, const void* q, const void* k_new, const void* v_new,
+                                void* k_cache, void* v_cache, const int32_t* block_tables, const int32_t* seq_lens,
+                                const int32_t* query_start_loc, const int32_t* seq_lens_host,
+                                const int32_t* query_start_loc_host, const int32_t* block_tables_host, void* out,
+                                float* lse, void* workspace, size_t workspace_bytes, void* stream);
+int mpa_append_prefill_attention(const mpa_shape* shape, const void* q, const void* k_new, const void* v_new,
+                                 void* k_cache, void* v_cache, const int32_t* block_tables, const int32_t* seq_lens,
+                                 const int32_t* query_start_loc, const int32_t* seq_lens_host,
+                                 const int32_t* query_start_loc_host, const int32_t* block_tables_host, void* out,
+                                 float* lse, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * The two halves of mpa_mixed_paged_attention, for callers that time them
  * separately or run them on two streams: mpa_decode_attention computes only
  * the rows of sequences with q_len == 1, mpa_prefill_attention only the rows

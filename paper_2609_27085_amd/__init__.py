@@ -36,6 +36,9 @@ BLOCK_SIZE = 16
 EXPORTS = (
     "mpa_kv_append",
     "mpa_mixed_paged_attention",
+    "mpa_append_attention",
+    "mpa_append_decode_attention",
+    "mpa_append_prefill_attention",
     "mpa_workspace_size",
     "mpa_status_string",
     "mpa_get_plan_info",
@@ -147,6 +150,12 @@ def lib() -> ctypes.CDLL:
         L.mpa_mixed_paged_attention.restype = ctypes.c_int
         L.mpa_mixed_paged_attention.argtypes = [
             _SHP, _P, _P, _P, _P, _P, _P, _I32P, _I32P, _I32P, _P, _P, _P, ctypes.c_size_t, _P]
+        L.mpa_append_attention.restype = ctypes.c_int
+        L.mpa_append_attention.argtypes = [
+            _SHP, _P, _P, _P, _P, _P, _P, _P, _P, _I32P, _I32P, _I32P, _P, _P, _P, ctypes.c_size_t, _P]
+        for name in ("mpa_append_decode_attention", "mpa_append_prefill_attention"):
+            getattr(L, name).restype = ctypes.c_int
+            getattr(L, name).argtypes = L.mpa_append_attention.argtypes
         L.mpa_decode_attention.restype = ctypes.c_int
         L.mpa_decode_attention.argtypes = L.mpa_mixed_paged_attention.argtypes
         L.mpa_prefill_attention.restype = ctypes.c_int
@@ -388,6 +397,27 @@ def mixed_paged_attention(q, k_cache, v_cache, block_tables, seq_lens, query_sta
     the scales of uint8 = fp8 caches)."""
     _attention("mpa_mixed_paged_attention", q, k_cache, v_cache, block_tables, seq_lens, query_start_loc,
                seq_lens_host, qsl_host, out, lse, workspace, scale, block_tables_host, stream, k_scale, v_scale)
+
+
+def append_attention(q, k_new, v_new, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host,
+                     qsl_host, out, lse=None, workspace=None, scale=None, block_tables_host=None, stream=None,
+                     k_scale=1.0, v_scale=1.0, which="mpa_append_attention") -> None:
+    """mpa_append_attention: kv_append then mixed_paged_attention in one call
+    (the decode rows' new tokens written by the decode kernel); `which` names
+    one of its halves instead (mpa_append_decode_attention,
+    mpa_append_prefill_attention)."""
+    if which not in ("mpa_append_attention", "mpa_append_decode_attention", "mpa_append_prefill_attention"):
+        raise ValueError(which)
+    sl, qs = _host_i32(seq_lens_host), _host_i32(qsl_host)
+    bth = None if block_tables_host is None else _host_i32(block_tables_host)
+    shape = shape_of(q, k_cache, block_tables, sl, scale, k_scale, v_scale)
+    args = [ctypes.byref(shape), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(block_tables),
+            _ptr(seq_lens), _ptr(query_start_loc), _i32p(sl), _i32p(qs), _i32p(bth), _ptr(out), _ptr(lse)]
+    args += [None, 0] if workspace is None else [_ptr(workspace), workspace.numel() * workspace.element_size()]
+    args.append(_stream(stream))
+    rc = getattr(lib(), which)(*args)
+    if rc != MPA_OK:
+        raise MpaError(rc, which)
 
 
 def decode_attention(q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host,

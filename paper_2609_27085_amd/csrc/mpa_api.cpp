@@ -360,7 +360,7 @@ int check_append_slots(const mpa_shape* sh, const int32_t* seq_lens, const int32
 int run_append(const mpa_shape* shape, const void* k_new, const void* v_new, void* k_cache, void* v_cache,
                const int32_t* block_tables, const int32_t* seq_lens, const int32_t* query_start_loc,
                const int32_t* seq_lens_host, const int32_t* query_start_loc_host, const int32_t* block_tables_host,
-               const mpa::RopeArgs* rope, void* stream) {
+               const mpa::RopeArgs* rope, void* stream, bool multi_only = false) {
   Batch b;
   int rc = check_batch(shape, seq_lens_host, query_start_loc_host, block_tables_host, true, &b);
   if (rc != MPA_OK) return rc;
@@ -388,6 +388,7 @@ int run_append(const mpa_shape* shape, const void* k_new, const void* v_new, voi
   // (which also rotates q, token by token) every sequence
   std::vector<int> seqs(b.decode);
   if (rope) seqs.insert(seqs.end(), b.prefill.begin(), b.prefill.end());
+  if (multi_only) seqs.clear();  // the decode kernel appends the single-token rows
   clear_stale_hip_error();
   // multi-token sequences one wave per (cache block, KV head)
   if (!rope) {
@@ -735,7 +736,8 @@ int run_attention(int phases, const mpa_shape* shape, const void* q, const void*
                   const int32_t* block_tables, const int32_t* seq_lens, const int32_t* query_start_loc,
                   const int32_t* seq_lens_host, const int32_t* query_start_loc_host,
                   const int32_t* block_tables_host, void* out, float* lse, void* workspace,
-                  size_t workspace_bytes_given, void* stream) {
+                  size_t workspace_bytes_given, void* stream, const void* k_new = nullptr,
+                  const void* v_new = nullptr, bool validate_only = false) {
   Batch b;
   int rc = check_batch(shape, seq_lens_host, query_start_loc_host, block_tables_host, false, &b);
   if (rc != MPA_OK) return rc;
@@ -783,6 +785,11 @@ int run_attention(int phases, const mpa_shape* shape, const void* q, const void*
   const bool fp8 = shape->dtype == MPA_FP8;
   a.scale_log2 = shape->scale * 1.4426950408889634f * (fp8 ? shape->k_scale : 1.f);
   a.v_scale = fp8 ? shape->v_scale : 1.f;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.inv_k_scale = fp8 ? 1.f / shape->k_scale : 1.f;
+  a.inv_v_scale = fp8 ? 1.f / shape->v_scale : 1.f;
+  if (validate_only) return MPA_OK;
   hipStream_t st = (hipStream_t)stream;
   clear_stale_hip_error();
 
@@ -886,6 +893,34 @@ int run_attention(int phases, const mpa_shape* shape, const void* q, const void*
   return MPA_OK;
 }
 
+// The append and the attention of the rows in `phases`, in one call: the
+// attention's checks (the workspace included) and the append's run first,
+// so an error means nothing was launched; then the multi-token rows' block
+// append (prefill phase), and the attention, whose decode kernel writes the
+// decode rows' new tokens itself.
+int run_fused(int phases, const mpa_shape* shape, const void* q, const void* k_new, const void* v_new,
+              void* k_cache, void* v_cache, const int32_t* block_tables, const int32_t* seq_lens,
+              const int32_t* query_start_loc, const int32_t* seq_lens_host, const int32_t* query_start_loc_host,
+              const int32_t* block_tables_host, void* out, float* lse, void* workspace, size_t workspace_bytes_given,
+              void* stream) {
+  int rc = run_attention(phases, shape, q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host,
+                         query_start_loc_host, block_tables_host, out, lse, workspace, workspace_bytes_given, stream,
+                         nullptr, nullptr, true);
+  if (rc != MPA_OK) return rc;
+  if (shape->total_q_tokens > 0 && (!k_new || !v_new)) return MPA_ERR_INVALID;
+  if (phases & kPrefill) {
+    rc = run_append(shape, k_new, v_new, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host,
+                    query_start_loc_host, block_tables_host, nullptr, stream, true);
+    if (rc != MPA_OK) return rc;
+  } else if (debug_checks()) {
+    rc = check_append_slots(shape, seq_lens_host, query_start_loc_host, block_tables_host);
+    if (rc != MPA_OK) return rc;
+  }
+  return run_attention(phases, shape, q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host,
+                       query_start_loc_host, block_tables_host, out, lse, workspace, workspace_bytes_given, stream,
+                       k_new, v_new);
+}
+
 }  // namespace
 
 extern "C" {
@@ -898,6 +933,36 @@ int mpa_mixed_paged_attention(const mpa_shape* shape, const void* q, const void*
   return run_attention(kDecode | kPrefill, shape, q, k_cache, v_cache, block_tables, seq_lens, query_start_loc,
                        seq_lens_host, query_start_loc_host, block_tables_host, out, lse, workspace,
                        workspace_bytes_given, stream);
+}
+
+int mpa_append_attention(const mpa_shape* shape, const void* q, const void* k_new, const void* v_new,
+                         void* k_cache, void* v_cache, const int32_t* block_tables, const int32_t* seq_lens,
+                         const int32_t* query_start_loc, const int32_t* seq_lens_host,
+                         const int32_t* query_start_loc_host, const int32_t* block_tables_host, void* out,
+                         float* lse, void* workspace, size_t workspace_bytes_given, void* stream) {
+  return run_fused(kDecode | kPrefill, shape, q, k_new, v_new, k_cache, v_cache, block_tables, seq_lens,
+                   query_start_loc, seq_lens_host, query_start_loc_host, block_tables_host, out, lse, workspace,
+                   workspace_bytes_given, stream);
+}
+
+int mpa_append_decode_attention(const mpa_shape* shape, const void* q, const void* k_new, const void* v_new,
+                                void* k_cache, void* v_cache, const int32_t* block_tables, const int32_t* seq_lens,
+                                const int32_t* query_start_loc, const int32_t* seq_lens_host,
+                                const int32_t* query_start_loc_host, const int32_t* block_tables_host, void* out,
+                                float* lse, void* workspace, size_t workspace_bytes_given, void* stream) {
+  return run_fused(kDecode, shape, q, k_new, v_new, k_cache, v_cache, block_tables, seq_lens, query_start_loc,
+                   seq_lens_host, query_start_loc_host, block_tables_host, out, lse, workspace,
+                   workspace_bytes_given, stream);
+}
+
+int mpa_append_prefill_attention(const mpa_shape* shape, const void* q, const void* k_new, const void* v_new,
+                                 void* k_cache, void* v_cache, const int32_t* block_tables, const int32_t* seq_lens,
+                                 const int32_t* query_start_loc, const int32_t* seq_lens_host,
+                                 const int32_t* query_start_loc_host, const int32_t* block_tables_host, void* out,
+                                 float* lse, void* workspace, size_t workspace_bytes_given, void* stream) {
+  return run_fused(kPrefill, shape, q, k_new, v_new, k_cache, v_cache, block_tables, seq_lens, query_start_loc,
+                   seq_lens_host, query_start_loc_host, block_tables_host, out, lse, workspace,
+                   workspace_bytes_given, stream);
 }
 
 int mpa_decode_attention(const mpa_shape* shape, const void* q, const void* k_cache, const void* v_cache,

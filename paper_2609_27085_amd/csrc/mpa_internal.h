@@ -33,6 +33,12 @@ struct AttnArgs {
   int32_t hq, hkv, mb, nb;
   float scale_log2;  // softmax scale * log2(e) (* the key scale for fp8 caches)
   float v_scale;     // fp8 caches: the value scale (1 otherwise), applied to outputs and partials
+  // Decode rows' appends folded into the decode kernel (null: none).  The
+  // wave that reads a decode row's last split first writes the row's new K
+  // and V ([T][Hkv][d], query row order) for its KV head into the cache.
+  const void* k_new;
+  const void* v_new;
+  float inv_k_scale, inv_v_scale;  // fp8 caches: 1 / scale, rounded to f32 (1 otherwise)
 };
 
 // Decode work for up to kMaxPlanSeqs sequences: item k of this launch is

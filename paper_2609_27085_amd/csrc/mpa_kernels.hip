@@ -423,6 +423,54 @@ __device__ inline void attend_blocks(const AttnArgs& a, const typename Tr<DT>::C
   }
 }
 
+template <int D>
+__device__ inline void store_fp8_chunk(const AppendArgs& a, size_t head, int c, int slot, u32x4 kw, u32x4 vw);
+
+// A decode row's new token (query row t, position pos) for KV head g,
+// written by the wave that reads the row's last split -- split edges are
+// block-aligned, so no other wave reads this (block, head) granule -- with
+// the bits the append kernels store (E4M3 codes for fp8 caches).  The wave
+// then waits for its stores before it loads any block.  A bad block id
+// writes nothing (the row comes out NaN).
+template <int DT, int D>
+__device__ inline void append_decode_token(const AttnArgs& a, int s, int pos, int t, int g) {
+  using T = Tr<DT>;
+  using E = typename T::Elem;
+  constexpr int X = T::X;
+  const int lane = threadIdx.x & 63;
+  const int blk = a.block_tables[(size_t)s * a.mb + pos / kBlock];
+  if (blk < 0 || blk >= a.nb) return;
+  const int slot = pos % kBlock;
+  const size_t head = (size_t)blk * a.hkv + g;
+  if constexpr (DT == 2) {
+    AppendArgs aa;
+    aa.k_cache = const_cast<void*>(a.k_cache);
+    aa.v_cache = const_cast<void*>(a.v_cache);
+    aa.inv_k_scale = a.inv_k_scale;
+    aa.inv_v_scale = a.inv_v_scale;
+    const uint16_t* kn = reinterpret_cast<const uint16_t*>(a.k_new) + ((size_t)t * a.hkv + g) * D;
+    const uint16_t* vn = reinterpret_cast<const uint16_t*>(a.v_new) + ((size_t)t * a.hkv + g) * D;
+    for (int c = lane; c < D / 8; c += 64)
+      store_fp8_chunk<D>(aa, head, c, slot, *reinterpret_cast<const u32x4*>(kn + c * 8),
+                         *reinterpret_cast<const u32x4*>(vn + c * 8));
+  } else {
+    constexpr int NC = D / X;
+    const size_t src = ((size_t)t * a.hkv + g) * D;
+    for (int c = lane; c < NC; c += 64) {
+      const u32x4 kv = *reinterpret_cast<const u32x4*>(reinterpret_cast<const E*>(a.k_new) + src + c * X);
+      E vv[X];
+#pragma unroll
+      for (int e = 0; e < X; ++e) vv[e] = reinterpret_cast<const E*>(a.v_new)[src + c * X + e];
+      *reinterpret_cast<u32x4*>(reinterpret_cast<E*>(const_cast<void*>(a.k_cache)) +
+                                ((head * NC + c) * kBlock + slot) * X) = kv;
+      E* vc = reinterpret_cast<E*>(const_cast<void*>(a.v_cache)) + (head * D + c * X) * kBlock + slot;
+#pragma unroll
+      for (int e = 0; e < X; ++e) vc[e * kBlock] = vv[e];
+    }
+  }
+  MPA_WAIT_VMCNT(0);  // stores are counted in vmcnt: complete before the first block load
+}
+
 // ---------------------------------------------------------------------------
 // Decode: one wave per (sequence, split, KV head); the G query heads of the
 // group are the 16 MFMA columns (columns >= G carry zero queries).
@@ -451,6 +499,7 @@ __global__ __launch_bounds__(256) void decode_kernel(AttnArgs a, DecodePlan p) {
   const int n = lane & 15, grp = lane >> 4;
   const bool head_ok = n < G;
   const int h = g * G + (head_ok ? n : 0);
+  if (a.k_new != nullptr && split == nsplit - 1) append_decode_token<DT, D>(a, s, L - 1, trow, g);
 
   const QE* q = reinterpret_cast<const QE*>(a.q) + ((size_t)trow * a.hq + h) * D;
   typename T::Chunk qf[R];

@@ -44,10 +44,20 @@ def say(*a):
     sys.stdout.flush()
 
 
-def run_step(d, lse=True, append=True):
-    """append + attention on the GPU; returns (out, lse) device tensors."""
+def run_step(d, lse=True, append=True, fused=False):
+    """append + attention on the GPU (two calls, or the one
+    mpa_append_attention call when fused); returns (out, lse) device tensors."""
     import torch
 
+    if fused:
+        out = torch.full_like(d.q, float("nan"))
+        l = torch.full(d.q.shape[:2], float("nan"), dtype=torch.float32, device=d.q.device) if lse else None
+        ws = mpa.alloc_workspace(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.qsl_host, d.scale)
+        mpa.append_attention(d.q, d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens,
+                             d.query_start_loc, d.seq_lens_host, d.qsl_host, out, lse=l, workspace=ws, scale=d.scale,
+                             block_tables_host=d.block_tables_host, k_scale=d.k_scale, v_scale=d.v_scale)
+        torch.cuda.synchronize()
+        return out, l
     if append:
         mpa.kv_append(d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
                       d.seq_lens_host, d.qsl_host, block_tables_host=d.block_tables_host, k_scale=d.k_scale,
@@ -84,11 +94,11 @@ def assert_close(got, exp, dtype, what=""):
     assert err.mean() <= mean, f"{what}: mean err {err.mean():.3g} > {mean}"
 
 
-def check_batch(b, what):
+def check_batch(b, what, fused=False):
     """Full parity of one host batch (append bit-exact + attention)."""
-    say(f"[gpu] {what}: S={b.num_seqs} T={b.total_q} heads={b.heads} dtype={b.dtype}")
+    say(f"[gpu] {what}: S={b.num_seqs} T={b.total_q} heads={b.heads} dtype={b.dtype} fused={fused}")
     d = to_device(b)
-    out, lse = run_step(d)
+    out, lse = run_step(d, fused=fused)
     kc, vc = ref.append_reference(b.k_cache, b.v_cache, b.k_new, b.v_new, b.block_tables, b.seq_lens,
                                   b.query_start_loc, b.heads.block_size, b.dtype, k_scale=b.k_scale,
                                   v_scale=b.v_scale)
@@ -553,3 +563,75 @@ def test_full_size_sampled(torch_gpu, name, dtype, tp):
         assert np.abs(lg[g_rows] - l_ref).max() <= LSE_TOL["bf16"]
     del d
     torch.cuda.empty_cache()
+
+
+# ----------------------------------------------------------------------------
+# mpa_append_attention: the append and the attention in one call, the decode
+# rows' new tokens written by the decode kernel
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32", "fp8"])
+@pytest.mark.parametrize("case", ["tiny", "mixed", "split", "boundaries"])
+def test_fused_append_attention(torch_gpu, dtype, case):
+    """Whole-batch parity of the fused call (cache bit-exact against the
+    oracle's append, attention to the bars), and bit-identity with the two
+    separate calls on the same batch: cache, out and lse."""
+    rng = np.random.default_rng(300 + len(case))
+    if case == "tiny":
+        b = config_batch("tiny", 1, dtype)
+    elif case == "mixed":
+        b = make_batch(mixed_specs(rng), HeadSpec(32, 8, 128 if dtype != "f32" else 64, 16), dtype, rng)
+    elif case == "split":
+        b = make_batch(split_specs(rng), HeadSpec(12, 4, 128, 16), dtype, rng)
+    else:  # multi-token appends at every slot alignment beside decode rows of many splits
+        specs = [SeqSpec(p + c, c) for p in (0, 1, 15, 16, 17) for c in (2, 16, 17)]
+        specs += [SeqSpec(int(L), 1) for L in (1, 16, 17, 1000, 4097, 9000)]
+        b = make_batch([specs[i] for i in rng.permutation(len(specs))], HeadSpec(8, 2, 64), dtype, rng)
+    d1, out1, lse1 = check_batch(b, f"fused {case}", fused=True)
+    d2 = to_device(b)
+    out2, lse2 = run_step(d2)
+    assert tensor_to_raw(d1.k_cache, b.dtype).tobytes() == tensor_to_raw(d2.k_cache, b.dtype).tobytes()
+    assert tensor_to_raw(d1.v_cache, b.dtype).tobytes() == tensor_to_raw(d2.v_cache, b.dtype).tobytes()
+    rows = torch_gpu.from_numpy(np.repeat(b.q_lens > 0, b.q_lens)).cuda()
+    assert torch_gpu.equal(out1[rows], out2[rows]) and torch_gpu.equal(lse1[rows], lse2[rows])
+    # its two halves, concurrently on two streams: the same bits again
+    torch = torch_gpu
+    d3 = to_device(b)
+    out3 = torch.full_like(d3.q, float("nan"))
+    lse3 = torch.full(d3.q.shape[:2], float("nan"), dtype=torch.float32, device=d3.q.device)
+    ws = mpa.alloc_workspace(d3.q, d3.k_cache, d3.block_tables, d3.seq_lens_host, d3.qsl_host, d3.scale)
+    main, side = torch.cuda.current_stream(), torch.cuda.Stream()
+    side.wait_stream(main)
+    for which, st in (("mpa_append_prefill_attention", side), ("mpa_append_decode_attention", main)):
+        mpa.append_attention(d3.q, d3.k_new, d3.v_new, d3.k_cache, d3.v_cache, d3.block_tables, d3.seq_lens,
+                             d3.query_start_loc, d3.seq_lens_host, d3.qsl_host, out3, lse=lse3, workspace=ws,
+                             scale=d3.scale, stream=st, k_scale=d3.k_scale, v_scale=d3.v_scale, which=which)
+    main.wait_stream(side)
+    torch.cuda.synchronize()
+    assert tensor_to_raw(d3.k_cache, b.dtype).tobytes() == tensor_to_raw(d2.k_cache, b.dtype).tobytes()
+    assert tensor_to_raw(d3.v_cache, b.dtype).tobytes() == tensor_to_raw(d2.v_cache, b.dtype).tobytes()
+    assert torch.equal(out3[rows], out2[rows]) and torch.equal(lse3[rows], lse2[rows])
+
+
+def test_fused_many_sequences_and_errors(torch_gpu):
+    """More than 256 decode rows (several decode launches, each appending its
+    own rows), and a too-small workspace: an error with nothing launched,
+    the cache untouched."""
+    import torch
+
+    rng = np.random.default_rng(310)
+    specs = [SeqSpec(int(c), 1) for c in rng.integers(1, 3000, size=300)] + [SeqSpec(500 + 70, 70)]
+    b = make_batch([specs[i] for i in rng.permutation(len(specs))], HeadSpec(16, 4, 128), "bf16", rng)
+    check_batch(b, "fused 301 sequences", fused=True)
+    d = to_device(b)
+    k0 = d.k_cache.clone()
+    ws = mpa.alloc_workspace(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.qsl_host, d.scale)
+    assert ws is not None and ws.numel() > 64
+    out = torch.empty_like(d.q)
+    with pytest.raises(mpa.MpaError) as e:
+        mpa.append_attention(d.q, d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens,
+                             d.query_start_loc, d.seq_lens_host, d.qsl_host, out, workspace=ws[:-64], scale=d.scale)
+    assert e.value.status == mpa.MPA_ERR_WORKSPACE
+    torch.cuda.synchronize()
+    # bits, not values: the pool holds NaN sentinels
+    assert torch.equal(d.k_cache.view(torch.int16), k0.view(torch.int16))

@@ -306,3 +306,24 @@ def test_plan_memo_matches_fresh_planning(monkeypatch):
     monkeypatch.delenv("MPA_SPLIT_TOKENS")
     monkeypatch.delenv("MPA_PREFILL_SPLITS")
     assert plan(a) == pa
+
+
+def test_append_attention_rejects_before_launch():
+    """mpa_append_attention runs every check of both calls before its first
+    launch: missing new rows, a short workspace and a malformed batch are
+    errors here, on a host without a GPU, where any launch would fail."""
+    L = mpa.lib()
+    sh = shape(max_blocks_per_seq=1024)
+    sl = np.asarray([9000, 40], np.int32)
+    qs = np.asarray([0, 1, 5], np.int32)
+    n = mpa.workspace_size(sh, sl, qs)
+
+    def rc(k_new, ws_ptr, ws, qsl=qs):
+        return L.mpa_append_attention(ctypes.byref(sh), FAKE, k_new, k_new, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                      mpa._i32p(sl), mpa._i32p(np.asarray(qsl, np.int32)), None, FAKE, None, ws_ptr,
+                                      ws, None)
+
+    assert rc(None, FAKE, n) == mpa.MPA_ERR_INVALID
+    assert rc(FAKE, FAKE, n - 1) == mpa.MPA_ERR_WORKSPACE
+    assert rc(FAKE, FAKE + 8, n + 64) == mpa.MPA_ERR_WORKSPACE
+    assert rc(FAKE, FAKE, n, qsl=[0, 2, 1]) == mpa.MPA_ERR_INVALID
