@@ -1,5 +1,6 @@
 """HIP-graph capture of a whole step: mpa_kv_append then
-mpa_mixed_paged_attention recorded once into a graph (through torch's graph
+mpa_mixed_paged_attention (or the one mpa_append_attention call) recorded
+once into a graph (through torch's graph
 capture on the library's stream argument) and replayed.
 
 Every launch takes its plan as kernel arguments and the library enqueues no
@@ -39,18 +40,26 @@ def graph_specs(rng):
     return [specs[i] for i in order]
 
 
+@pytest.mark.parametrize("fused", [False, True], ids=["two_calls", "one_call"])
 @pytest.mark.parametrize("heads", [(32, 8, 128), (8, 2, 64)], ids=lambda h: f"hq{h[0]}_hkv{h[1]}_d{h[2]}")
-def test_graph_replays_equal_eager_step(torch_gpu, heads):
+def test_graph_replays_equal_eager_step(torch_gpu, heads, fused):
+    """The step as mpa_kv_append + mpa_mixed_paged_attention, or as the one
+    mpa_append_attention call (whose decode kernel writes the new tokens)."""
     torch = torch_gpu
     rng = np.random.default_rng(60 + heads[2])
     b = make_batch(graph_specs(rng), HeadSpec(*heads, 16), "bf16", rng)
-    print(f"[gpu] graph capture: S={b.num_seqs} T={b.total_q} heads={heads}", flush=True)
+    print(f"[gpu] graph capture: S={b.num_seqs} T={b.total_q} heads={heads} fused={fused}", flush=True)
     d = to_device(b)
     ws = mpa.alloc_workspace(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.qsl_host, d.scale)
     out = torch.full_like(d.q, float("nan"))
     lse = torch.full(d.q.shape[:2], float("nan"), dtype=torch.float32, device="cuda")
 
     def step():
+        if fused:
+            mpa.append_attention(d.q, d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens,
+                                 d.query_start_loc, d.seq_lens_host, d.qsl_host, out, lse=lse, workspace=ws,
+                                 scale=d.scale)
+            return
         mpa.kv_append(d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
                       d.seq_lens_host, d.qsl_host)
         mpa.mixed_paged_attention(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc,
