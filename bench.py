@@ -12,7 +12,8 @@ before timing starts.  Prints one JSON line:
   value          query tokens/s over the timed steps (T * steps / wall time)
   roofline       the dominant phase's algorithmic bytes (or FLOPs) per launch
                  over its average duration, timed with HIP events around that
-                 phase in every timed step, against the MI355X datasheet peak
+                 phase in every 4th timed step (--event-every), against the
+                 MI355X datasheet peak
                  (HBM 8 TB/s, bf16 dense MFMA 2.5 PF)
   phases_ms      every phase's duration from an untimed calibration pass with
                  events between all phases (each event record costs ~4 us of
@@ -257,6 +258,9 @@ def main(argv=None) -> int:
                     help="fused (default): the append inside the attention calls (mpa_append_prefill_attention, "
                          "mpa_append_decode_attention: the decode kernel writes the decode rows' new tokens); "
                          "separate: mpa_kv_append, then the attention")
+    ap.add_argument("--event-every", type=int, default=4, metavar="N",
+                    help="record the HIP events around the dominant phase on every N-th timed step (default 4; "
+                         "1: every step); the roofline averages those steps")
     ap.add_argument("--flush-mb", type=int, default=0, metavar="MB",
                     help="read MB megabytes of device memory before every timed step (cache flush) and time each "
                          "step with events; value then comes from the median step (default 0: back-to-back steps, "
@@ -409,11 +413,15 @@ def main(argv=None) -> int:
         value = work["query_tokens"] / (ms_per_step * 1e-3)
         del flush
     else:
-        events = [new_events(dom_marks) for _ in range(args.steps)]
+        # the two events around the dominant phase on every event_every-th
+        # timed step (each record costs ~3.4 us of GPU time)
+        timed_ks = list(range(0, args.steps, max(1, args.event_every)))
+        events = [new_events(dom_marks) for _ in timed_ks]
+        ev_at = dict(zip(timed_ks, events))
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for k in range(args.steps):
-            step(events[k])
+            step(ev_at.get(k))
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
         ms_per_step = wall * 1e3 / args.steps
@@ -463,7 +471,8 @@ def main(argv=None) -> int:
                    "append": ("fused into the attention halves (decode rows by the decode kernel)" if fused
                               else "mpa_kv_append before the attention"),
                    "timing": (f"median of per-step events, {args.flush_mb} MB device read before each step"
-                              if args.flush_mb else "wall clock over back-to-back steps"),
+                              if args.flush_mb else "wall clock over back-to-back steps; roofline events on every "
+                              f"{max(1, args.event_every)}th step"),
                    "kv_cache": "bf16" if args.kv == "bf16" else "fp8 e4m3 (per-cache scale)",
                    "decode_rows": work["decode_rows"], "prefill_chunks": work["prefill_chunks"],
                    "query_tokens": work["query_tokens"],
