@@ -95,11 +95,33 @@ def _quantize_truncating(y32):
 _good_e4m3 = ref.e4m3_values
 
 
+def _round_bf16_truncating(x32):
+    # wrong: drops the low 16 bits of the float32 instead of rounding them
+    return (np.ascontiguousarray(x32, dtype=np.float32).view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+
+
+def _round_bf16_ties_away(x32):
+    # wrong: rounds ties away from zero instead of to the even pattern
+    u = np.ascontiguousarray(x32, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    r = ((u + np.uint64(0x8000)) >> np.uint64(16)).astype(np.uint16)
+    nan = np.isnan(x32)
+    r[nan] = 0x7FC0
+    return r
+
+
+def _fp8_codes_times_scale(x_raw_bf16, scale):
+    # wrong: multiplies by the scale instead of by its reciprocal
+    return ref.quantize_e4m3(ref.decode_raw(x_raw_bf16, "bf16").astype(np.float32) * np.float32(scale))
+
+
 MUTANTS = {
     "rope_interleaved_pairs": ("rope_reference", _rope_interleaved),
     "rope_reversed": ("rope_reference", _rope_sign),
     "e4m3_fnuz_bias": ("e4m3_values", _e4m3_fnuz_values),
     "e4m3_truncating": ("quantize_e4m3", _quantize_truncating),
+    "round_bf16_truncating": ("round_bf16", _round_bf16_truncating),
+    "round_bf16_ties_away": ("round_bf16", _round_bf16_ties_away),
+    "fp8_codes_times_scale": ("fp8_codes", _fp8_codes_times_scale),
     "top_left_causal": ("sequence_attention", _seq_attn_factory(
         visible_fn=lambda keys, rows, prefix: keys[None] <= rows[:, None])),
     "exclusive_diagonal": ("sequence_attention", _seq_attn_factory(
@@ -121,6 +143,9 @@ PIN_TESTS = [
     lambda: pins.test_rope_zero_and_quarter_turn("f32"),
     lambda: pins.test_e4m3_table_fixed_points(),
     lambda: pins.test_e4m3_quantize_round_trip_ties_and_saturation(),
+    lambda: pins.test_round_bf16_ties_carries_and_nan(),
+    lambda: pins.test_rope_bf16_rounding_hand_worked(),
+    lambda: pins.test_fp8_codes_scale_direction_and_round_trip(),
 ]
 
 

@@ -419,6 +419,38 @@ def test_bf16_decode_and_rounding():
     assert np.array_equal(bf16_bits_from_f32(x), tb)
 
 
+def test_round_bf16_ties_carries_and_nan():
+    """The oracle's float32 -> bf16 rounding (used for the rotary output),
+    against values worked out by hand from round-to-nearest-even on the top
+    16 bits of the float32 pattern, and against torch's conversion."""
+    pat = np.array([
+        0x3F808000,  # 1 + 2^-8: a tie, the even pattern 0x3F80 stays
+        0x3F818000,  # 1 + 3*2^-8: a tie, up to the even 0x3F82
+        0xBF808000,  # -(1 + 2^-8): a tie, the sign kept
+        0x3F808008,  # just above the tie of 1 + 2^-8: up
+        0x3F807FFF,  # just below it: down
+        0x3F7F8000,  # 1 - 2^-9: a tie from the odd 0x3F7F, carries into the exponent (1.0)
+        0x3FFFFFFF,  # just under 2: carries into the exponent (2.0)
+        0x00008000,  # a subnormal tie: to +0
+        0x00018000,  # a subnormal tie from an odd pattern: up to 0x0002
+        0x7F7FFFFF,  # the largest float32: past the largest bf16, to +inf
+        0xFF800000,  # -inf stays
+        0x7F800001,  # a signalling NaN whose payload sits in the low bits only: stays a NaN
+        0xFFC00000,  # a negative quiet NaN
+    ], np.uint32)
+    got = ref.round_bf16(pat.view(np.float32))
+    assert got.tolist() == [0x3F80, 0x3F82, 0xBF80, 0x3F81, 0x3F80, 0x3F80, 0x4000, 0x0000, 0x0002, 0x7F80, 0xFF80,
+                            0x7FC0, 0xFFC0]
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(13)
+    x = (rng.standard_normal(100000) * 100).astype(np.float32)
+    ties = (rng.integers(0, 0x7F000000, size=20000, dtype=np.uint32) & np.uint32(0xFFFF0000)) | np.uint32(0x8000)
+    ties |= (rng.random(20000) < 0.5).astype(np.uint32) << np.uint32(31)
+    x = np.concatenate([x, ties.view(np.float32)])
+    tb = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(ref.round_bf16(x), tb)
+
+
 # ----------------------------------------------------------------------------
 # rotary position embedding (the append step's optional rotation)
 
@@ -442,6 +474,25 @@ def test_rope_hand_worked():
     y = ref.rope_reference(x, [0], cs[:, :2], 4, "f32")
     assert y.ravel().tolist() == [1 * .5 - 3 * .25, 2 * .5 - 4 * .25, 3 * .5 + 1 * .25, 4 * .5 + 2 * .25,
                                   5, 6, 7, 8]
+
+
+def test_rope_bf16_rounding_hand_worked():
+    """A bf16 rotation whose float32 products, sum and bf16 result all need
+    rounding, worked by hand (R = d = 2: one pair, x = (3, 5); the table holds
+    float32 0.6 and 0.8):
+      c = fl(0.6) = 10066330 * 2^-24, s = fl(0.8) = 13421773 * 2^-24;
+      fl(3c) = 15099495 * 2^-23 (exact), fl(5s) = 4 (67108865 * 2^-24 rounded);
+      y0 = fl(fl(3c) - 4) = -18454937 * 2^-23, a float32 tie, to -9227468 * 2^-22;
+           bf16: 140.8 units of 2^-6, so -141 * 2^-6 = -2.203125 (0xC00D);
+      fl(5c) = 3 (50331650 * 2^-24, a tie to even), fl(3s) = 10066330 * 2^-22;
+      y1 = 3 + fl(3s) = 11324621 * 2^-21, exact; bf16: 172.8 units of 2^-5,
+           so 173 * 2^-5 = 5.40625 (0x40AD).
+    And with the table (1 + 2^-8, 2^-9) on x = (1, 1): y0 = 1 + 2^-9 rounds
+    down to 1.0 (0x3F80), y1 = 1 + 3 * 2^-9 up to 1 + 2^-7 (0x3F81)."""
+    x = np.array([[[0x4040, 0x40A0]], [[0x3F80, 0x3F80]]], np.uint16)
+    cs = np.array([[[0.6, 0.8]], [[1 + 2 ** -8, 2 ** -9]]], np.float32)
+    y = ref.rope_reference(x, [0, 1], cs, 2, "bf16")
+    assert y.reshape(2, 2).tolist() == [[0xC00D, 0x40AD], [0x3F80, 0x3F81]]
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
@@ -510,6 +561,28 @@ def test_e4m3_quantize_round_trip_ties_and_saturation():
     y = np.sort(np.random.default_rng(50).standard_normal(20000).astype(np.float32) * 100)
     c = ref.quantize_e4m3(y)
     assert np.all(np.diff(v[c]) >= 0)  # monotone
+
+
+def test_fp8_codes_scale_direction_and_round_trip():
+    """fp8_codes stores x * (1 / scale).  Hand-worked: 1.0 at scale 0.5 is
+    2.0 = 1.0 * 2^1 (exponent field 8: 0x40); 1.0 at scale 2 is 0.5 (0x30);
+    3.0 at scale 0.25 is 12 = 1.5 * 2^3 (0x54); 1.0 at scale fl(0.3) is
+    3.3333333, nearer 3.25 = 1.625 * 2 (0x45) than 3.5; -1.0 at scale 0.5 is
+    -2.0 (0xC0).  Then every finite code c survives the trip through its
+    value times a non-unit scale, rounded to bf16: codes are 2^-4 apart
+    relative to their value (2^-9 absolute below 2^-6), far wider than the
+    2^-9 relative error of the bf16 rounding."""
+    one, three, minus = 0x3F80, 0x4040, 0xBF80
+    assert ref.fp8_codes(np.array([one], np.uint16), 0.5).tolist() == [0x40]
+    assert ref.fp8_codes(np.array([one], np.uint16), 2.0).tolist() == [0x30]
+    assert ref.fp8_codes(np.array([three], np.uint16), 0.25).tolist() == [0x54]
+    assert ref.fp8_codes(np.array([one], np.uint16), 0.3).tolist() == [0x45]
+    assert ref.fp8_codes(np.array([minus], np.uint16), 0.5).tolist() == [0xC0]
+    v = ref.e4m3_values()
+    finite = np.array([c for c in range(256) if not np.isnan(v[c])], np.uint8)
+    for scale in (0.5, 0.0173, 3.7):
+        x = bf16_bits_from_f32((v[finite] * scale).astype(np.float32))
+        assert np.array_equal(ref.fp8_codes(x, scale), finite), scale
 
 
 def test_e4m3_matches_torch_in_range():
