@@ -149,6 +149,10 @@ int env_int(const char* name) {
 
 PlanMemo& plan_memo(const mpa_shape* sh, const int32_t* seq_lens, const int32_t* qsl) {
   thread_local PlanMemo m;
+  // an empty batch may come without metadata (check_batch accepts null
+  // arrays when num_seqs is 0): its query_start_loc is {0}
+  static const int32_t kEmptyQsl[1] = {0};
+  if (sh->num_seqs == 0 && !qsl) qsl = kEmptyQsl;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess) dev = -1;
   const int32_t key[7] = {sh->num_q_heads, sh->num_kv_heads, sh->head_dim, (int32_t)sh->dtype, dev,

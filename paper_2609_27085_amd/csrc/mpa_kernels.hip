@@ -698,11 +698,15 @@ __global__ __launch_bounds__(256) void prefill_kernel(AttnArgs a, PrefillPlan p)
   if (first_tok + (wave * 16) / G >= C) return;  // this wave has no rows
   const int n = lane & 15, grp = lane >> 4;
   const int row = wave * 16 + n;
-  const int i_raw = first_tok + row / G;
-  const bool row_ok = i_raw < C;
-  const int i = row_ok ? i_raw : C - 1;
+  // The tile holds q_tile tokens (G * q_tile <= 64 rows): when G does not
+  // divide 64, the last rows of the workgroup would fall on the next tile's
+  // first token.  They compute a valid token of this tile and store nothing.
+  const int r_tok = row / G;
+  const int i_raw = first_tok + min(r_tok, p.q_tile - 1);
+  const bool row_ok = r_tok < p.q_tile && i_raw < C;
+  const int i = min(i_raw, C - 1);
   const int h = g * G + row % G;
-  const int last_tok = min(first_tok + (wave * 16 + 15) / G, C - 1);
+  const int last_tok = min(first_tok + min((wave * 16 + 15) / G, p.q_tile - 1), C - 1);
   const int kend = P + last_tok + 1;  // keys this wave needs
 
   const QE* q = reinterpret_cast<const QE*>(a.q) + ((size_t)(t0 + i) * a.hq + h) * D;
@@ -810,18 +814,22 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   const int ntile = split == nsplit - 1 ? (kend + BN - 1) / BN : kt_begin + p.split_tiles[j];
   cint* bt = (cint*)(a.block_tables + (size_t)s * a.mb);
 
-  // this lane's query row
+  // this lane's query row.  The tile holds q_tile tokens (G * q_tile <= 256
+  // rows): when G does not divide 256, the last rows of the workgroup would
+  // fall on the next tile's first token, past the keys loaded here.  They
+  // compute a valid token of this tile and store nothing.
   const int n = lane & 31, h = lane >> 5;
   const int row = wave * 32 + n;
-  const int i_raw = first_tok + row / G;
-  const bool row_ok = i_raw < C;
-  const int i = row_ok ? i_raw : C - 1;
+  const int r_tok = row / G;
+  const int i_raw = first_tok + min(r_tok, p.q_tile - 1);
+  const bool row_ok = r_tok < p.q_tile && i_raw < C;
+  const int i = min(i_raw, C - 1);
   const int head = g * G + row % G;
   const int limit = P + i;
   const int w_first = first_tok + (wave * 32) / G;
   const bool wave_active = w_first < C;
   const int w_min_limit = P + min(w_first, C - 1);
-  const int w_kend = P + min(first_tok + (wave * 32 + 31) / G, C - 1) + 1;
+  const int w_kend = P + min(first_tok + min((wave * 32 + 31) / G, p.q_tile - 1), C - 1) + 1;
 
   bf16x8 qf[KS];
   {

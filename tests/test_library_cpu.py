@@ -327,3 +327,28 @@ def test_append_attention_rejects_before_launch():
     assert rc(FAKE, FAKE, n - 1) == mpa.MPA_ERR_WORKSPACE
     assert rc(FAKE, FAKE + 8, n + 64) == mpa.MPA_ERR_WORKSPACE
     assert rc(FAKE, FAKE, n, qsl=[0, 2, 1]) == mpa.MPA_ERR_INVALID
+
+
+def test_empty_batch_without_metadata():
+    """An empty step (num_seqs 0) may come with null seq_lens and
+    query_start_loc: every planning entry point answers it, and the step's
+    calls return ok without launching anything (there is no GPU here)."""
+    L = mpa.lib()
+    sh = mpa.make_shape(num_seqs=0, num_q_heads=8, num_kv_heads=2, head_dim=128, num_blocks=0, max_blocks_per_seq=0,
+                        total_q_tokens=0, scale=0.1, dtype=mpa.MPA_BF16)
+    assert L.mpa_workspace_size(ctypes.byref(sh), None, None) == 0
+    info = mpa.MpaPlanInfo()
+    assert L.mpa_get_plan_info(ctypes.byref(sh), None, None, ctypes.byref(info)) == mpa.MPA_OK
+    assert info.num_decode_seqs == 0 and info.num_prefill_seqs == 0 and info.num_prefill_tiles == 0
+    t = mpa.MpaStepTime()
+    assert L.mpa_predict_step(ctypes.byref(sh), None, None, None, ctypes.byref(t)) == mpa.MPA_OK
+    assert t.step_us == 0.0
+    mode = ctypes.c_int32(-1)
+    assert L.mpa_plan_coexec(ctypes.byref(sh), None, None, None, ctypes.byref(mode), None) == mpa.MPA_OK
+    assert mode.value == 0
+    assert L.mpa_kv_append(ctypes.byref(sh), None, None, None, None, None, None, None, None, None, None,
+                           None) == mpa.MPA_OK
+    assert L.mpa_mixed_paged_attention(ctypes.byref(sh), None, None, None, None, None, None, None, None, None,
+                                       None, None, None, 0, None) == mpa.MPA_OK
+    assert L.mpa_append_attention(ctypes.byref(sh), None, None, None, None, None, None, None, None, None, None,
+                                  None, None, None, None, 0, None) == mpa.MPA_OK
