@@ -9,16 +9,19 @@ mpa_append_decode_attention, whose decode kernel writes the decode rows' new
 tokens); --append separate calls mpa_kv_append first.  Inputs are synthetic and resident in HBM
 before timing starts.  Prints one JSON line:
 
-  value          query tokens/s over the timed steps (T * steps / wall time)
-  roofline       the dominant phase's algorithmic bytes (or FLOPs) per launch
-                 over its average duration, timed with HIP events around that
-                 phase in every 4th timed step (--event-every), against the
-                 MI355X datasheet peak
+  value          query tokens/s: T / step time, the median step of the timed
+                 steps, each preceded by a 512 MB streaming read of device
+                 memory (a cache flush) and bracketed by its own two events
+                 (--flush-mb 0: wall clock over back-to-back steps)
+  roofline       the dominant half's algorithmic bytes (or FLOPs) per launch
+                 over its average duration: --phase-reps back-to-back launches
+                 of that half's attention call alone (no append), between one
+                 event pair on its stream, against the MI355X datasheet peak
                  (HBM 8 TB/s, bf16 dense MFMA 2.5 PF)
-  phases_ms      every phase's duration from an untimed calibration pass with
-                 events between all phases (each event record costs ~4 us of
-                 GPU time, so the timed steps carry only the two around the
-                 dominant phase)
+  decode_hbm_gbs, prefill_tflops
+                 the same for each half present
+  phases_ms      every phase of the step from an untimed calibration pass with
+                 events between all phases
   step_roofline  max(t_mem, t_mfma) / step time and (t_mem + t_mfma) / step time,
                  t_mem and t_mfma being the step's algorithmic bytes at 8 TB/s and
                  FLOPs at 2.5 PF
@@ -28,7 +31,7 @@ before timing starts.  Prints one JSON line:
                  read, dense bf16 MFMA) and the roofline's fraction of that
   cpu_baseline   the CPU oracle, timed on a bounded sample of the same step
 
-    python bench.py [--steps K] [--warmup W] [--config decode8b] [--seed 0]
+    python bench.py [--steps K] [--warmup W] [--config longctx] [--seed 0]
 """
 
 from __future__ import annotations
@@ -234,9 +237,9 @@ def measured_peaks(torch, mpa, read_bytes: int = 2 << 30, mfma_iters: int = 2000
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", default="decode8b", choices=sorted(WORKLOADS))
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="longctx", choices=sorted(WORKLOADS))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -258,13 +261,13 @@ def main(argv=None) -> int:
                     help="fused (default): the append inside the attention calls (mpa_append_prefill_attention, "
                          "mpa_append_decode_attention: the decode kernel writes the decode rows' new tokens); "
                          "separate: mpa_kv_append, then the attention")
-    ap.add_argument("--event-every", type=int, default=4, metavar="N",
-                    help="record the HIP events around the dominant phase on every N-th timed step (default 4; "
-                         "1: every step); the roofline averages those steps")
-    ap.add_argument("--flush-mb", type=int, default=0, metavar="MB",
+    ap.add_argument("--flush-mb", type=int, default=512, metavar="MB",
                     help="read MB megabytes of device memory before every timed step (cache flush) and time each "
-                         "step with events; value then comes from the median step (default 0: back-to-back steps, "
-                         "wall clock)")
+                         "step with its own events; value comes from the median step (default 512; 0: back-to-back "
+                         "steps, wall clock)")
+    ap.add_argument("--phase-reps", type=int, default=10, metavar="N",
+                    help="back-to-back launches of each attention half alone (after two untimed ones), between one "
+                         "event pair on its stream: the phase rates and the roofline (default 10)")
     ap.add_argument("--graph", action="store_true",
                     help="also capture one step into a HIP graph (torch.cuda.graph) and time its replays")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -299,10 +302,6 @@ def main(argv=None) -> int:
     work = algorithmic_work(d.seq_lens_host, d.qsl_host, heads.num_q_heads, heads.num_kv_heads, heads.head_dim, 2,
                             kv_bytes=1 if args.kv == "fp8" else 2)
     fused = args.append == "fused"
-    if fused:  # the decode rows' new K/V are read and written inside the decode phase
-        moved = 2 * work["decode_rows"] * heads.num_kv_heads * heads.head_dim * (2 + (1 if args.kv == "fp8" else 2))
-        work["decode_bytes"] += moved
-        work["append_bytes"] -= moved
     sc = dict(k_scale=d.k_scale, v_scale=d.v_scale)
     ws = mpa.alloc_workspace(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.qsl_host, d.scale)
     out = torch.empty_like(d.q)
@@ -385,14 +384,12 @@ def main(argv=None) -> int:
 
     for _ in range(args.warmup):
         step()
-    # untimed calibration pass: every phase, to pick the dominant one
+    # untimed calibration pass: every phase of the step, events between them
     calib = [new_events(["start", "append", "prefill", "decode", "end"]) for _ in range(max(3, min(10, args.steps)))]
     for e in calib:
         step(e)
     torch.cuda.synchronize()
     phase_ms = {k: avg_ms(calib, k) for k in spans}
-    dom = "decode" if has_dec and (not has_pre or phase_ms["decode"] >= phase_ms["prefill"]) else "prefill"
-    dom_marks = list(spans[dom])
 
     if args.flush_mb:
         # a streaming read of flush_mb MB before every timed step, which
@@ -403,7 +400,7 @@ def main(argv=None) -> int:
         flush = torch.zeros(args.flush_mb << 20, dtype=torch.uint8, device="cuda")
         sink = torch.zeros(4, dtype=torch.uint8, device="cuda")
         mpa.probe_stream_read(flush, sink)
-        events = [new_events(sorted(set(dom_marks) | {"start", "end"})) for _ in range(args.steps)]
+        events = [new_events(["start", "end"]) for _ in range(args.steps)]
         torch.cuda.synchronize()
         for k in range(args.steps):
             mpa.probe_stream_read(flush, sink)
@@ -413,31 +410,62 @@ def main(argv=None) -> int:
         value = work["query_tokens"] / (ms_per_step * 1e-3)
         del flush
     else:
-        # the two events around the dominant phase on every event_every-th
-        # timed step (each record costs ~3.4 us of GPU time)
-        timed_ks = list(range(0, args.steps, max(1, args.event_every)))
-        events = [new_events(dom_marks) for _ in timed_ks]
-        ev_at = dict(zip(timed_ks, events))
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        for k in range(args.steps):
-            step(ev_at.get(k))
+        for _ in range(args.steps):
+            step()
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
         ms_per_step = wall * 1e3 / args.steps
         value = work["query_tokens"] * args.steps / wall
-    dom_ms = avg_ms(events, dom)
-    # the dominant phase from the timed steps, the other from the calibration pass
-    timed = dict(phase_ms)
-    timed[dom] = dom_ms
-    dec_gbs = work["decode_bytes"] / (timed["decode"] * 1e-3) / 1e9 if has_dec else None
-    pre_tflops = work["prefill_flops"] / (timed["prefill"] * 1e-3) / 1e12 if has_pre else None
+
+    # Each half's attention call alone (no append): phase_reps launches back
+    # to back between one event pair on the stream they run on (a partition
+    # stream in co-execution mode), after two untimed launches.
+    def half_alone_ms(which):
+        fn = mpa.decode_attention if which == "decode" else mpa.prefill_attention
+        st = torch.cuda.current_stream()
+        if part:
+            st = part[0] if which == "decode" else part[1]
+
+        def launch():
+            fn(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc, d.seq_lens_host,
+               d.qsl_host, out, lse=lse, workspace=ws, scale=d.scale, stream=st, **sc)
+
+        for _ in range(2):
+            launch()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(st)
+        for _ in range(max(1, args.phase_reps)):
+            launch()
+        b.record(st)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / max(1, args.phase_reps)
+
+    alone = {}
+    if has_dec:
+        alone["decode"] = half_alone_ms("decode")
+    if has_pre:
+        alone["prefill"] = half_alone_ms("prefill")
+    dom = max(alone, key=alone.get)
+    dom_ms = alone[dom]
+    dec_gbs = work["decode_bytes"] / (alone["decode"] * 1e-3) / 1e9 if has_dec else None
+    pre_tflops = work["prefill_flops"] / (alone["prefill"] * 1e-3) / 1e12 if has_pre else None
+    info = mpa.plan_info(mpa.shape_of(d.q, d.k_cache, d.block_tables, d.seq_lens_host, d.scale, **sc),
+                         d.seq_lens_host, d.qsl_host)
     if dom == "decode":
         achieved, peak, unit, bound = dec_gbs, HBM_PEAK_GBS, "GB/s", "hbm"
-        kernel = "decode_kernel+merge_kernel"
+        split_rows = any(-(-int(L) // info.split_tokens) > 1
+                         for L, c in zip(d.seq_lens_host, np.diff(d.qsl_host)) if c == 1)
+        kernel = "decode_kernel+merge_kernel" if split_rows else "decode_kernel"
     else:
         achieved, peak, unit, bound = pre_tflops, MFMA_BF16_PEAK_TFLOPS, "TFLOP/s", "mfma"
         kernel = "prefill_mfma_kernel"
+        if info.prefill_max_splits > 1:
+            kernel += "+prefill_merge_kernel"
+        if any(int(L) - int(c) < 64 for L, c in zip(d.seq_lens_host, np.diff(d.qsl_host)) if c > 1):
+            kernel += "+prefill_kernel (rows of at most 64 keys)"
     roofline = {
         "bound": bound,
         "achieved": round(achieved, 2),
@@ -447,7 +475,9 @@ def main(argv=None) -> int:
         "traffic": measured_traffic(args.config, dom) if args.kv == "bf16" and args.tp == 1 else None,
         "kernel": kernel,
         "phase_ms": round(dom_ms, 4),
-        "algorithmic_per_launch": work[f"{dom}_bytes"] if dom == "decode" else work["prefill_flops"],
+        "algorithmic_per_launch": work["decode_bytes"] if dom == "decode" else work["prefill_flops"],
+        "how": f"{max(1, args.phase_reps)} back-to-back launches of mpa_{dom}_attention alone (no append) between "
+               "one event pair on its stream, after two untimed launches",
     }
     total_bytes = work["decode_bytes"] + work["prefill_bytes"] + work["append_bytes"]
     total_flops = work["decode_flops"] + work["prefill_flops"]
@@ -462,7 +492,7 @@ def main(argv=None) -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "bf16" if args.kv == "bf16" else "fp8",
         "data": "synthetic (seeded N(0,1) values, shuffled block tables)",
         "config": {"workload": f"{args.config}: {WORKLOADS[args.config]}"
                                + (f"; one GPU's share of TP{args.tp}: {heads.num_q_heads}/{heads.num_kv_heads} heads"
@@ -470,16 +500,17 @@ def main(argv=None) -> int:
                    "seed": args.seed, "streams": args.streams if two else 1,
                    "append": ("fused into the attention halves (decode rows by the decode kernel)" if fused
                               else "mpa_kv_append before the attention"),
-                   "timing": (f"median of per-step events, {args.flush_mb} MB device read before each step"
-                              if args.flush_mb else "wall clock over back-to-back steps; roofline events on every "
-                              f"{max(1, args.event_every)}th step"),
-                   "kv_cache": "bf16" if args.kv == "bf16" else "fp8 e4m3 (per-cache scale)",
+                   "timing": (f"median of {args.steps} steps, each between its own two events after a "
+                              f"{args.flush_mb} MB device read" if args.flush_mb
+                              else "wall clock over back-to-back steps"),
+                   "kv_cache": "bf16" if args.kv == "bf16" else "fp8 e4m3 (per-cache scale; bf16 MFMA on the codes)",
                    "decode_rows": work["decode_rows"], "prefill_chunks": work["prefill_chunks"],
                    "query_tokens": work["query_tokens"],
                    "parallelism": f"one GPU's share of tp{args.tp}" if args.tp > 1 else "single GPU",
                    "exec": f"decode on {coexec_mode}/4 of every XCD beside prefill" if coexec_mode else "one stream"},
         "roofline": roofline,
         "phases_ms": {k: round(v, 4) for k, v in phase_ms.items()},
+        "halves_alone_ms": {k: round(v, 4) for k, v in alone.items()},
         "decode_hbm_gbs": round(dec_gbs, 1) if dec_gbs else None,
         "decode_hbm_frac": round(dec_gbs / HBM_PEAK_GBS, 4) if dec_gbs else None,
         "prefill_tflops": round(pre_tflops, 2) if pre_tflops else None,

@@ -32,3 +32,8 @@ def test_bench_line(extra):
     cb = line["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["value"] > 0 and cb["cores"] >= 1 and cb["sample"]
     assert "workload" in line["config"]
+    if not extra:
+        assert line["config"]["workload"].startswith("longctx") and rf["bound"] == "mfma"
+    # the dominant half alone cannot take longer than the whole step
+    assert rf["phase_ms"] <= line["ms_per_step"] * 1.02
+    assert line["dtype"] == "bf16"

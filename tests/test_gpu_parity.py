@@ -248,6 +248,32 @@ def test_prefill_kv_splits(torch_gpu, heads, dtype):
     check_batch(b, f"kv splits {heads} {dtype}")
 
 
+# Group sizes that do not divide a prefill workgroup's rows (256 for the MFMA
+# kernel, 64 for the generic one): a tile holds q_tile = rows // G tokens and
+# the last rows of the workgroup are left over.  Chunks on prefixes P with
+# P + q_tile a multiple of 16 (and of 64) put the next tile's first key on a
+# block (and key-tile) boundary, where a leftover row computed as that token
+# would read a block the workgroup never loaded.
+RAGGED_G = [
+    ((12, 4, 128), [(91, 100), (11, 100), (107, 100), (1035, 100)]),  # G 3, q_tile 85 (MFMA) / 21 (generic)
+    ((24, 4, 128), [(86, 100), (1030, 100), (6, 100)]),               # G 6, q_tile 42 / 10
+    ((28, 4, 64), [(92, 100), (1036, 100), (3, 100)]),                # G 7, q_tile 36 / 9
+]
+
+
+@pytest.mark.parametrize("splits", ["1", "4"])
+@pytest.mark.parametrize("dtype", ["bf16", "fp8", "f32"])
+@pytest.mark.parametrize("heads,chunks", RAGGED_G, ids=lambda x: f"hq{x[0]}_hkv{x[1]}_d{x[2]}" if len(x) == 3 else "")
+def test_group_sizes_not_dividing_the_tile(torch_gpu, heads, chunks, dtype, splits, monkeypatch):
+    if dtype == "f32" and splits != "1":
+        pytest.skip("f32 chunks are never KV-split")
+    monkeypatch.setenv("MPA_PREFILL_SPLITS", splits)
+    rng = np.random.default_rng(90 + heads[0])
+    specs = [SeqSpec(p + c, c) for p, c in chunks] + [SeqSpec(int(L), 1) for L in rng.integers(1, 3000, size=3)]
+    b = make_batch([specs[i] for i in rng.permutation(len(specs))], HeadSpec(*heads, 16), dtype, rng)
+    check_batch(b, f"ragged G {heads} {dtype} splits={splits}")
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "fp8"])
 def test_decode_split_boundaries(torch_gpu, dtype, monkeypatch):
     """Decode rows whose lengths sit at and around multiples of a forced
@@ -366,6 +392,42 @@ def test_fp8_append_rounding_edges(torch_gpu):
                                   b.query_start_loc, 16, "fp8", k_scale=1.0, v_scale=1.0)
     assert tensor_to_raw(d.k_cache, "fp8").tobytes() == kc.tobytes()
     assert tensor_to_raw(d.v_cache, "fp8").tobytes() == vc.tobytes()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+@pytest.mark.parametrize("heads", [(32, 8, 128), (8, 2, 64)], ids=lambda h: f"hq{h[0]}_hkv{h[1]}_d{h[2]}")
+def test_decode_row_equals_last_chunk_row(torch_gpu, dtype, heads):
+    """A decode row (one query at position L - 1) and the last row of a
+    prefill chunk that ends at the same position see the same keys: the
+    decode kernel (split-K, merged) and the prefill kernel (MFMA tiles, KV
+    split or not) must agree on it, to the bf16 bars, and both match the
+    oracle.  The chunk's step appends the keys; the decode call then reads
+    the same cache through the same block table."""
+    import torch
+
+    rng = np.random.default_rng(95 + heads[2])
+    specs = [SeqSpec(3000, 100), SeqSpec(700, 333), SeqSpec(20000, 300), SeqSpec(5000, 64)]
+    b = make_batch(specs, HeadSpec(*heads, 16), dtype, rng)
+    d, out, lse = check_batch(b, f"chunks for the decode-row property {heads} {dtype}")
+    for s, sp in enumerate(specs):
+        last = int(b.query_start_loc[s + 1]) - 1
+        qd = d.q[last:last + 1].contiguous()
+        sl = np.array([sp.ctx], np.int32)
+        qs = np.array([0, 1], np.int32)
+        o1 = torch.full_like(qd, float("nan"))
+        l1 = torch.full(qd.shape[:2], float("nan"), dtype=torch.float32, device="cuda")
+        bt = d.block_tables[s:s + 1].contiguous()
+        seq_lens = torch.from_numpy(sl).cuda()
+        qsl = torch.from_numpy(qs).cuda()
+        ws = mpa.alloc_workspace(qd, d.k_cache, bt, sl, qs, d.scale)
+        mpa.mixed_paged_attention(qd, d.k_cache, d.v_cache, bt, seq_lens, qsl, sl, qs, o1, lse=l1, workspace=ws,
+                                  scale=d.scale, block_tables_host=d.block_tables_host[s:s + 1], k_scale=d.k_scale,
+                                  v_scale=d.v_scale)
+        torch.cuda.synchronize()
+        a, c = as_f64(o1)[0], as_f64(out)[last]
+        err = np.abs(a - c)
+        assert err.max() <= 1e-2 and err.mean() <= 1e-3, f"seq {s}: decode vs chunk row {err.max():.3g}"
+        assert np.abs(l1.cpu().numpy()[0] - lse.cpu().numpy()[last]).max() <= 2 * LSE_TOL[dtype]
 
 
 def test_block_permutation_bit_identical(torch_gpu):
@@ -531,15 +593,35 @@ FULL = ["decode8b", "lent", "agentic", "budget0", "budget256", "budget1024", "bu
 FULL_TP4 = ["decode8b", "agentic", "budget256", "longctx"]
 
 
-@pytest.mark.parametrize("name,dtype,tp", [(n, "bf16", 1) for n in FULL] + [("decode8b", "fp8", 1), ("lent", "fp8", 1)]
-                         + [(n, "bf16", 4) for n in FULL_TP4],
-                         ids=lambda x: x if isinstance(x, str) else f"tp{x}")
-def test_full_size_sampled(torch_gpu, name, dtype, tp):
+# the workloads whose shape changes most with the seed (agentic's class flips
+# between HBM- and MFMA-bound), at seeds 1-4 as well
+FULL_SEEDS = ["agentic", "lent", "longctx", "budget4096"]
+
+FULL_CASES = ([(n, "bf16", 1, 0) for n in FULL] + [("decode8b", "fp8", 1, 0), ("lent", "fp8", 1, 0)]
+              + [(n, "bf16", 4, 0) for n in FULL_TP4]
+              + [(n, "bf16", 1, s) for n in FULL_SEEDS for s in (1, 2, 3, 4)]
+              + [("decode8b", "fp8", 1, 1), ("lent", "fp8", 1, 1)])
+
+
+def post_append_blocks(d, seqs):
+    """The cache blocks of chosen sequences, as raw host arrays in the order
+    host_subbatch lays them out (sequence by sequence, logical block order)."""
     import torch
 
-    seed = 0
+    bs = d.heads.block_size
+    blocks = np.concatenate([d.block_tables_host[s, :-(-int(d.seq_lens_host[s]) // bs)] for s in seqs])
+    idx = torch.from_numpy(blocks.astype(np.int64)).to(d.k_cache.device)
+    return (tensor_to_raw(d.k_cache.index_select(0, idx), d.dtype),
+            tensor_to_raw(d.v_cache.index_select(0, idx), d.dtype))
+
+
+@pytest.mark.parametrize("name,dtype,tp,seed", FULL_CASES,
+                         ids=lambda x: x if isinstance(x, str) else None)
+def test_full_size_sampled(torch_gpu, name, dtype, tp, seed):
+    import torch
+
     specs, heads, nb, rng = config_specs(name, seed, tp=tp)
-    say(f"[gpu] full size {name} {dtype} tp{tp}: {len(specs)} seqs, T={sum(s.q_len for s in specs)}, "
+    say(f"[gpu] full size {name} {dtype} tp{tp} seed {seed}: {len(specs)} seqs, T={sum(s.q_len for s in specs)}, "
         f"{heads.num_q_heads}/{heads.num_kv_heads} heads")
     d = device_step(specs, heads, dtype, rng, seed, num_blocks=nb)
     srng = np.random.default_rng(1000 + seed)
@@ -551,6 +633,12 @@ def test_full_size_sampled(torch_gpu, name, dtype, tp):
     sub = host_subbatch(d, pick)  # pre-append contents
     b = sub["batch"]
     out, lse = run_step(d, fused=True)  # the one-call step bench.py times
+    # the sampled sequences' blocks after the step: the oracle's append, bit for bit
+    kc, vc = ref.append_reference(b.k_cache, b.v_cache, b.k_new, b.v_new, b.block_tables, b.seq_lens,
+                                  b.query_start_loc, b.heads.block_size, b.dtype, k_scale=b.k_scale,
+                                  v_scale=b.v_scale)
+    kg, vg = post_append_blocks(d, pick)
+    assert kg.tobytes() == kc.tobytes() and vg.tobytes() == vc.tobytes(), f"{name} seed {seed}: append"
     got = as_f64(out)
     lg = lse.cpu().numpy().astype(np.float64)
     assert np.isfinite(got).all()
