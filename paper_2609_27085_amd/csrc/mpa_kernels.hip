@@ -69,6 +69,14 @@ constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) |
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(n));      \
     asm volatile("" ::: "memory");                 \
   } while (0)
+// The same for the LDS / scalar-memory counter (vmcnt and expcnt left at
+// their maxima).
+constexpr int lgkmcnt_imm(int n) { return 15 | (7 << 4) | ((n & 15) << 8) | (3 << 14); }
+#define MPA_WAIT_LGKMCNT(n)                        \
+  do {                                             \
+    __builtin_amdgcn_s_waitcnt(lgkmcnt_imm(n));    \
+    asm volatile("" ::: "memory");                 \
+  } while (0)
 
 // 16 bytes per lane from global memory straight into LDS: lane l reads the
 // 16 bytes at base + voff (base uniform, held in SGPRs; voff the lane's byte
@@ -1072,6 +1080,11 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
     } else {
       copy_tile(kt + AHEAD, cblk);
       next_blk = tile_block(kt + AHEAD + 1);
+      // The block id is a scalar load, which shares the LDS counter and may
+      // return out of order.  Left pending on this path, it would reach the
+      // active path's join as well, and every wait for the K operand reads
+      // there would become a wait for all of them.
+      MPA_WAIT_LGKMCNT(0);
     }
     if constexpr (CT == 2) {
       // this lane's pieces of tile kt+1 (the only loads in flight)
