@@ -89,8 +89,12 @@ typedef enum {
   MPA_ERR_INVALID = -1,     /* malformed arguments or batch metadata */
   MPA_ERR_UNSUPPORTED = -2, /* a shape or dtype this build does not handle */
   MPA_ERR_WORKSPACE = -3,   /* workspace missing, smaller than required or misaligned */
-  MPA_ERR_HIP = -4          /* a HIP launch reported an error */
+  MPA_ERR_HIP = -4,         /* a HIP launch reported an error */
+  MPA_ERR_SCRATCH = -5      /* mpa_append_attention_noalloc: the batch needs more than MPA_SCRATCH_BYTES */
 } mpa_status;
+
+/* Size of the library's fixed device array behind mpa_append_attention_noalloc. */
+#define MPA_SCRATCH_BYTES ((size_t)256 << 20)
 
 typedef enum { MPA_BF16 = 0, MPA_F32 = 1, MPA_FP8 = 2 } mpa_dtype;
 
@@ -238,6 +242,30 @@ int mpa_append_attention(const mpa_shape* shape, const void* q, const void* k_ne
                          const int32_t* query_start_loc, const int32_t* seq_lens_host,
                          const int32_t* query_start_loc_host, const int32_t* block_tables_host, void* out,
                          float* lse, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * mpa_append_attention without a workspace argument, for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc.  The step's split-K
+ * partial results live in a fixed device array inside the library,
+ * MPA_SCRATCH_BYTES (256 MiB) on each device the library runs on, held
+ * until the process ends; its device address is looked up (with
+ * hipGetSymbolAddress) on the first call on each device.  The call itself
+ * allocates no device memory.
+ *
+ * Arguments, results (bit-identical to mpa_append_attention) and checks as
+ * for mpa_append_attention.  A batch for which mpa_workspace_size exceeds
+ * MPA_SCRATCH_BYTES returns MPA_ERR_SCRATCH with nothing launched; use
+ * mpa_append_attention with a workspace for it.  Every call on a device
+ * shares that device's array: calls that overlap on one device (two
+ * streams, two threads) race on it and must be serialised by the caller.
+ * No part of the array needs to start at zero.
+ */
+int mpa_append_attention_noalloc(const mpa_shape* shape, const void* q, const void* k_new, const void* v_new,
+                                 void* k_cache, void* v_cache, const int32_t* block_tables, const int32_t* seq_lens,
+                                 const int32_t* query_start_loc, const int32_t* seq_lens_host,
+                                 const int32_t* query_start_loc_host, const int32_t* block_tables_host, void* out,
+                                 float* lse, void* stream);
 
 /*
  * The two halves of mpa_append_attention, as mpa_decode_attention and

@@ -28,6 +28,8 @@ MPA_ERR_INVALID = -1
 MPA_ERR_UNSUPPORTED = -2
 MPA_ERR_WORKSPACE = -3
 MPA_ERR_HIP = -4
+MPA_ERR_SCRATCH = -5
+MPA_SCRATCH_BYTES = 256 << 20  # the fixed device array behind mpa_append_attention_noalloc
 MPA_BF16 = 0
 MPA_F32 = 1
 MPA_FP8 = 2  # fp8 (OCP E4M3) caches with bf16 queries, new rows and outputs
@@ -39,6 +41,7 @@ EXPORTS = (
     "mpa_append_attention",
     "mpa_append_decode_attention",
     "mpa_append_prefill_attention",
+    "mpa_append_attention_noalloc",
     "mpa_workspace_size",
     "mpa_status_string",
     "mpa_get_plan_info",
@@ -153,6 +156,9 @@ def lib() -> ctypes.CDLL:
         L.mpa_append_attention.restype = ctypes.c_int
         L.mpa_append_attention.argtypes = [
             _SHP, _P, _P, _P, _P, _P, _P, _P, _P, _I32P, _I32P, _I32P, _P, _P, _P, ctypes.c_size_t, _P]
+        L.mpa_append_attention_noalloc.restype = ctypes.c_int
+        L.mpa_append_attention_noalloc.argtypes = [
+            _SHP, _P, _P, _P, _P, _P, _P, _P, _P, _I32P, _I32P, _I32P, _P, _P, _P]
         for name in ("mpa_append_decode_attention", "mpa_append_prefill_attention"):
             getattr(L, name).restype = ctypes.c_int
             getattr(L, name).argtypes = L.mpa_append_attention.argtypes
@@ -418,6 +424,22 @@ def append_attention(q, k_new, v_new, k_cache, v_cache, block_tables, seq_lens, 
     rc = getattr(lib(), which)(*args)
     if rc != MPA_OK:
         raise MpaError(rc, which)
+
+
+def append_attention_noalloc(q, k_new, v_new, k_cache, v_cache, block_tables, seq_lens, query_start_loc,
+                             seq_lens_host, qsl_host, out, lse=None, scale=None, block_tables_host=None, stream=None,
+                             k_scale=1.0, v_scale=1.0) -> None:
+    """mpa_append_attention_noalloc: the one-call step with its partial
+    results in the library's fixed device array (no workspace argument)."""
+    sl, qs = _host_i32(seq_lens_host), _host_i32(qsl_host)
+    bth = None if block_tables_host is None else _host_i32(block_tables_host)
+    shape = shape_of(q, k_cache, block_tables, sl, scale, k_scale, v_scale)
+    rc = lib().mpa_append_attention_noalloc(
+        ctypes.byref(shape), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(block_tables),
+        _ptr(seq_lens), _ptr(query_start_loc), _i32p(sl), _i32p(qs), _i32p(bth), _ptr(out), _ptr(lse),
+        _stream(stream))
+    if rc != MPA_OK:
+        raise MpaError(rc, "mpa_append_attention_noalloc")
 
 
 def decode_attention(q, k_cache, v_cache, block_tables, seq_lens, query_start_loc, seq_lens_host, qsl_host,

@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmpa.so")
-SOURCES = ["mpa_kernels.hip", "mpa_api.cpp", "mpa_probes.hip"]
+SOURCES = ["mpa_kernels.hip", "mpa_api.cpp", "mpa_probes.hip", "mpa_noalloc.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -518,6 +518,7 @@ const char* mpa_status_string(int status) {
     case MPA_ERR_UNSUPPORTED: return "unsupported shape or dtype";
     case MPA_ERR_WORKSPACE: return "workspace missing, too small or not 16-byte aligned";
     case MPA_ERR_HIP: return "HIP launch error";
+    case MPA_ERR_SCRATCH: return "batch needs more than the library's fixed scratch array (MPA_SCRATCH_BYTES)";
     default: return "unknown status";
   }
 }

@@ -51,7 +51,7 @@ def test_binding_signatures_match_header():
 
 
 def test_status_strings():
-    for code in (0, -1, -2, -3, -4):
+    for code in (0, -1, -2, -3, -4, -5):
         assert mpa.status_string(code)
     assert mpa.status_string(123) == "unknown status"
 
@@ -352,3 +352,21 @@ def test_empty_batch_without_metadata():
                                        None, None, None, 0, None) == mpa.MPA_OK
     assert L.mpa_append_attention(ctypes.byref(sh), None, None, None, None, None, None, None, None, None, None,
                                   None, None, None, None, 0, None) == mpa.MPA_OK
+
+
+def test_noalloc_refuses_batches_beyond_its_array():
+    """mpa_append_attention_noalloc: a batch whose partial results exceed
+    the fixed array is refused with MPA_ERR_SCRATCH before anything runs
+    (here no device exists), and the array's size is the header's."""
+    L = mpa.lib()
+    src = open(HEADER).read()
+    assert "#define MPA_SCRATCH_BYTES ((size_t)256 << 20)" in src and mpa.MPA_SCRATCH_BYTES == 256 << 20
+    sl = np.full(256, 32768, np.int32)
+    qs = np.arange(257, dtype=np.int32)
+    sh = mpa.make_shape(num_seqs=256, num_q_heads=64, num_kv_heads=8, head_dim=128, num_blocks=600000,
+                        max_blocks_per_seq=2048, total_q_tokens=256, scale=0.1, dtype=mpa.MPA_BF16)
+    assert mpa.workspace_size(sh, sl, qs) > mpa.MPA_SCRATCH_BYTES
+    rc = L.mpa_append_attention_noalloc(ctypes.byref(sh), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                        mpa._i32p(sl), mpa._i32p(qs), None, FAKE, None, None)
+    assert rc == mpa.MPA_ERR_SCRATCH
+    assert "scratch" in mpa.status_string(rc)
