@@ -7,7 +7,7 @@ first in the batch, prefill chunks after them.  "k" means 1024 throughout.
 
 The shapes stand in for the paper's workloads, which are traces that are not
 available here: up to 256 running requests and contexts up to 128K tokens on a
-decode worker (section 6.1), decode contexts of 65K-98K tokens (section 3.3),
+decode worker (section 6.1), decode contexts of 65K-98K tokens (section 3.2),
 prefill chunks on radix-cached prefixes (section 4.4, section 5), and a
 per-step prefill token budget as the lease's compute credit (section 4.2).
 
