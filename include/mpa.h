@@ -360,7 +360,8 @@ int mpa_get_plan_info(const mpa_shape* shape, const int32_t* seq_lens_host,
  *             launch with a KV-split chunk, prefill_merge_us +
  *             prefill_merge_row_us per partial (token, q head, split) row;
  *             plus prefill_fixup_us when a chunk sits on a prefix shorter
- *             than 64 tokens
+ *             than 64 tokens (its first key tile is passed twice for the
+ *             rows that see at most 64 keys; 0 in the default rates)
  *
  * Rates are in microseconds and GB/s (1e9 bytes/s).  mpa_default_rates
  * fills in figures measured on one MI355X with bench.py.  Only bf16 caches

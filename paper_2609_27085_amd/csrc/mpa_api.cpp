@@ -578,7 +578,9 @@ void mpa_default_rates(mpa_rates* r) {
   // lent and budget4096 at a quarter of the heads, where partitioning lost
   // 14-16 %)
   r->coexec_fixed_us = 80.0;
-  r->prefill_fixup_us = 8.0;
+  // the few-key rows' second pass over their first key tile adds less than
+  // a tile to one workgroup, which the makespan absorbs
+  r->prefill_fixup_us = 0.0;
   r->prefill_slots = 256;
   // CU-partitioned co-execution (mpa_plan_coexec), measured on agentic, lent
   // and budget4096, each half alone on its CU set: the decode half's speed
@@ -861,37 +863,6 @@ int run_attention(int phases, const mpa_shape* shape, const void* q, const void*
     if (e != hipSuccess) return MPA_ERR_HIP;
     if (rows > 0) {
       e = mpa::launch_prefill_merge(a, p, shape->dtype, shape->head_dim, st);
-      if (e != hipSuccess) return MPA_ERR_HIP;
-    }
-  }
-  // bf16 and fp8: the MFMA kernel rounds every probability to bf16, which averages
-  // out over many keys but not over a handful.  The rows that see at most
-  // kFewKeys keys (the first tokens of a chunk on a shorter prefix) are
-  // recomputed, after it on the same stream, by the generic kernel, which
-  // carries their probabilities to about 16 bits.
-  if (shape->dtype != MPA_F32) {
-    const int qg = mpa::kPrefillRows / (shape->num_q_heads / shape->num_kv_heads);
-    std::vector<std::pair<int, int>> few;  // (sequence, tiles of qg tokens)
-    for (int s : b.prefill) {
-      const int C = query_start_loc_host[s + 1] - query_start_loc_host[s];
-      const int P = seq_lens_host[s] - C;
-      if (P < mpa::kFewKeys) few.emplace_back(s, (std::min(C, mpa::kFewKeys - P) + qg - 1) / qg);
-    }
-    for (size_t c0 = 0; c0 < few.size(); c0 += mpa::kMaxPrefillSeqs) {
-      mpa::PrefillPlan p;
-      memset(&p, 0, sizeof(p));
-      const size_t c1 = std::min(few.size(), c0 + mpa::kMaxPrefillSeqs);
-      p.n_seqs = (int32_t)(c1 - c0);
-      p.q_tile = qg;
-      int acc = 0;
-      for (size_t k = c0; k < c1; ++k) {
-        p.seq[k - c0] = few[k].first;
-        p.tile_start[k - c0] = acc;
-        p.nsplit[k - c0] = 1;
-        acc += few[k].second;
-      }
-      p.tile_start[c1 - c0] = acc;
-      hipError_t e = mpa::launch_prefill_generic(a, p, acc, shape->dtype, shape->head_dim, st);
       if (e != hipSuccess) return MPA_ERR_HIP;
     }
   }

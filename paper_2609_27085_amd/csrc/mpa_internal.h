@@ -139,8 +139,6 @@ hipError_t launch_prefill(const AttnArgs& a, const PrefillPlan& p, int n_tiles, 
 // The generic (16 rows per wave) prefill kernel for any dtype; in bf16 it
 // recomputes the rows of a chunk that see at most 64 keys, after the MFMA
 // kernel, with the probabilities carried to about 16 bits.
-hipError_t launch_prefill_generic(const AttnArgs& a, const PrefillPlan& p, int n_tiles, int dtype, int head_dim,
-                                  hipStream_t stream);
 // Combines the KV-split partial results of the plan's split chunks.
 hipError_t launch_prefill_merge(const AttnArgs& a, const PrefillPlan& p, int dtype, int head_dim,
                                 hipStream_t stream);

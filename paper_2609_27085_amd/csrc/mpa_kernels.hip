@@ -1060,8 +1060,6 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
       const float mc = m_ref * c;
       // P^T in bf16; the row sum adds the rounded values the PV product
       // uses (four independent partial sums, two probabilities per dot2).
-      // Rows that see at most 64 keys are recomputed afterwards by the
-      // generic prefill kernel, which keeps P to about 16 bits for them.
       bf16x8 pb[4];
       float l4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -1077,6 +1075,58 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[t][dt], pb[t], o[dt], 0, 0, 0);
       l += (l4[0] + l4[1]) + (l4[2] + l4[3]);
+      if (key_base == 0 && w_min_limit < kFewKeys) {
+        // A row that sees at most kFewKeys keys has them all in tile 0, and
+        // its output rests on so few probabilities that their bf16 rounding
+        // does not average out.  For such waves the tile is passed a second
+        // time with the remainder p - bf16(p): S is recomputed from the
+        // operands still in LDS (the same products in the same order, so
+        // the same values), and the remainder goes into the PV product and
+        // the row sum, which carries P to about 16 bits.  The empty asm
+        // keeps the compiler from holding the first pass's fragments live
+        // across the tile for this rare branch.
+        asm volatile("" ::: "memory");
+        f32x16 s2[2];
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) s2[rt][r] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+          for (int rt = 0; rt < 2; ++rt)
+            s2[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8,
+                                   *reinterpret_cast<const u32x4*>(K + 2 * rt * BLK + koff + (2 * ks + h) * 128)),
+                qf[ks], s2[rt], 0, 0, 0);
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int jr = r >> 2;
+            const int key = 32 * rt + 16 * (jr >> 1) + 8 * h + 4 * (jr & 1) + (r & 3);
+            if (key > limit) s2[rt][r] = -INFINITY;
+          }
+        float r4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          bf16x8 plo;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float pe = exp2_fast(fmaf(s2[t >> 1][8 * (t & 1) + e], c, -mc));
+            plo[e] = (__bf16)(pe - (float)(__bf16)pe);
+          }
+          const u32x4 w = __builtin_bit_cast(u32x4, plo);
+#pragma unroll
+          for (int k = 0; k < 4; ++k) r4[k] = add_bf16_pair(w[k], r4[k]);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+            o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(V + t * BLK + (h * D + n) * 8 + 32 * dt * 8)),
+                plo, o[dt], 0, 0, 0);
+        }
+        l += (r4[0] + r4[1]) + (r4[2] + r4[3]);
+      }
     } else {
       copy_tile(kt + AHEAD, cblk);
       next_blk = tile_block(kt + AHEAD + 1);
@@ -1485,21 +1535,15 @@ hipError_t launch_prefill_mfma(const AttnArgs& a, const PrefillPlan& p, int n_ti
 
 // The generic prefill kernel for any dtype (the bf16 few-key pass).
 template <int DT, int D>
-struct PrefillGenericL {
-  static hipError_t run(const AttnArgs& a, const PrefillPlan& p, int n_tiles, hipStream_t stream) {
-    if (n_tiles == 0) return hipSuccess;
-    hipLaunchKernelGGL((prefill_kernel<DT, D>), dim3(n_tiles, a.hkv), dim3(64 * kWavesPerGroup), 0, stream, a, p);
-    return hipGetLastError();
-  }
-};
-
-template <int DT, int D>
 struct PrefillL {
   static hipError_t run(const AttnArgs& a, const PrefillPlan& p, int n_tiles, hipStream_t stream) {
     if (n_tiles == 0) return hipSuccess;
-    if constexpr (DT == 0 || DT == 2) return launch_prefill_mfma<DT, D>(a, p, n_tiles, stream);
-    hipLaunchKernelGGL((prefill_kernel<DT, D>), dim3(n_tiles, a.hkv), dim3(64 * kWavesPerGroup), 0, stream, a, p);
-    return hipGetLastError();
+    if constexpr (DT == 0 || DT == 2) {
+      return launch_prefill_mfma<DT, D>(a, p, n_tiles, stream);
+    } else {
+      hipLaunchKernelGGL((prefill_kernel<DT, D>), dim3(n_tiles, a.hkv), dim3(64 * kWavesPerGroup), 0, stream, a, p);
+      return hipGetLastError();
+    }
   }
 };
 
@@ -1576,11 +1620,6 @@ hipError_t launch_prefill_merge(const AttnArgs& a, const PrefillPlan& p, int dty
 hipError_t launch_prefill(const AttnArgs& a, const PrefillPlan& p, int n_tiles, int dtype, int head_dim,
                           hipStream_t stream) {
   return dispatch<PrefillL>(dtype, head_dim, a, p, n_tiles, stream);
-}
-
-hipError_t launch_prefill_generic(const AttnArgs& a, const PrefillPlan& p, int n_tiles, int dtype, int head_dim,
-                                  hipStream_t stream) {
-  return dispatch<PrefillGenericL>(dtype, head_dim, a, p, n_tiles, stream);
 }
 
 }  // namespace mpa
