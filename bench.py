@@ -230,7 +230,7 @@ def measured_peaks(torch, mpa, read_bytes: int = 2 << 30, mfma_iters: int = 2000
     del buf
     return {"stream_read_gbs": round(read_bytes / (read_ms * 1e-3) / 1e9, 1),
             "mfma_bf16_tflops": round(flops[-1] / (mfma_ms * 1e-3) / 1e12, 1),
-            "how": f"median of {reps}: one {read_bytes >> 20} MiB read with 16-byte loads; "
+            "how": f"median of {reps}: one {read_bytes >> 20} MiB read with 16-byte non-temporal loads; "
                    f"{mfma_iters} rounds of 4 independent 32x32x16 bf16 MFMAs in 4096 waves"}
 
 

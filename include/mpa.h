@@ -452,7 +452,7 @@ int mpa_partition_streams(int32_t mode, void** decode_stream, void** prefill_str
  * measured peak.  Both launch one kernel on `stream`, allocate nothing, and
  * return MPA_OK, MPA_ERR_INVALID (nothing launched) or MPA_ERR_HIP.
  *
- * mpa_probe_stream_read: reads every byte of buf once with 16-byte loads.
+ * mpa_probe_stream_read: reads every byte of buf once with 16-byte non-temporal loads.
  *   buf    device, 16-byte aligned, `bytes` long (a multiple of 16, > 0)
  *   sink   device uint32_t[1]; written only when the data's XOR hits one
  *          fixed value (it keeps the loads), so its contents are unspecified

@@ -563,8 +563,10 @@ void mpa_default_rates(mpa_rates* r) {
   r->append_gbs = 545.0;
   r->append_block_us = 17.0;
   r->append_block_gbs = 3700.0;
-  r->decode_fixed_us = 2.0;
-  r->decode_gbs = 5600.0;
+  // decode: refitted to the decode half alone after its cache reads became
+  // non-temporal (the fit puts the launch's fixed cost inside the rate)
+  r->decode_fixed_us = 0.0;
+  r->decode_gbs = 5880.0;
   r->decode_wave_gbs = 4.8;
   r->merge_us = 5.0;
   r->prefill_wg_us = 18.0;
@@ -573,30 +575,31 @@ void mpa_default_rates(mpa_rates* r) {
   r->prefill_merge_row_us = 1.6e-4;
   // A partitioned step's fixed cost beyond the model (the cross-stream waits,
   // and interference that the slowdown factor underrates on short steps):
-  // fitted with coexec_slowdown to the five partitioned steps measured
-  // against one stream (agentic and budget4096 at 64/8 and 32/8 heads, and
-  // lent and budget4096 at a quarter of the heads, where partitioning lost
-  // 14-16 %)
-  r->coexec_fixed_us = 80.0;
+  // fitted with coexec_slowdown, on a grid, to the four modes measured on
+  // agentic, lent, budget4096, budget1024 and longctx, and on the TP4 shares
+  // of agentic, lent and budget4096: the lowest mean regret of the
+  // planner's choice with no choice slower than one stream is at slowdown
+  // 1.10; the slowdown is one grid step above it (1.15), a margin for the
+  // few percent that step times move between devices
+  r->coexec_fixed_us = 130.0;
   // the few-key rows' second pass over their first key tile adds less than
   // a tile to one workgroup, which the makespan absorbs
   r->prefill_fixup_us = 0.0;
   r->prefill_slots = 256;
-  // CU-partitioned co-execution (mpa_plan_coexec), measured on agentic, lent
-  // and budget4096, each half alone on its CU set: the decode half's speed
-  // on 1, 2 and 3 quarters of every XCD's CUs relative to the whole device,
-  // the prefill half's likewise (faster than its share of the CUs: fewer
-  // CUs contend for the same HBM and L2), and the slowdown of the two halves
-  // side by side over the slower of them alone (shared HBM, L2 and MALL;
-  // 1.09-1.42 across the nine partitions, the decisions checked against all
-  // of them)
-  r->coexec_decode_q1 = 0.54;
-  r->coexec_decode_q2 = 0.85;
+  // CU-partitioned co-execution (mpa_plan_coexec), measured on agentic, lent,
+  // budget4096, budget1024 and longctx, each half alone on its CU set: the
+  // decode half's speed on 1, 2 and 3 quarters of every XCD's CUs relative
+  // to the whole device, the prefill half's likewise (faster than its share
+  // of the CUs: fewer CUs contend for the same HBM and L2), medians over the
+  // five; and the slowdown of the two halves side by side over the slower of
+  // them alone (shared HBM, L2 and MALL)
+  r->coexec_decode_q1 = 0.53;
+  r->coexec_decode_q2 = 0.83;
   r->coexec_decode_q3 = 1.0;
-  r->coexec_prefill_q1 = 0.335;
-  r->coexec_prefill_q2 = 0.62;
-  r->coexec_prefill_q3 = 0.77;
-  r->coexec_slowdown = 1.25;
+  r->coexec_prefill_q1 = 0.33;
+  r->coexec_prefill_q2 = 0.60;
+  r->coexec_prefill_q3 = 0.73;
+  r->coexec_slowdown = 1.15;
 }
 
 int mpa_predict_step(const mpa_shape* shape, const int32_t* seq_lens_host, const int32_t* qsl_host,

@@ -3,8 +3,9 @@
 // fraction of a measured peak beside the datasheet one.
 //
 //   mpa_probe_stream_read  HBM read bandwidth: every byte of a buffer is read
-//                          once with 16-byte vector loads, contiguous 4 KB
-//                          runs per workgroup.
+//                          once with 16-byte non-temporal vector loads,
+//                          contiguous 4 KB runs per workgroup (plain loads
+//                          sustain about a tenth less on gfx950).
 //   mpa_probe_mfma_bf16    dense bf16 matrix-core rate: independent chains of
 //                          v_mfma_f32_32x32x16_bf16 with operands in registers.
 //
@@ -40,7 +41,7 @@ __global__ __launch_bounds__(kReadThreads) void stream_read_kernel(const u32x4* 
 #pragma unroll
     for (int u = 0; u < kReadUnroll; ++u) {
       const size_t i = base + (size_t)u * kReadThreads + threadIdx.x;
-      v[u] = i < n16 ? src[i] : u32x4{0, 0, 0, 0};
+      v[u] = i < n16 ? __builtin_nontemporal_load(src + i) : u32x4{0, 0, 0, 0};
     }
 #pragma unroll
     for (int u = 0; u < kReadUnroll; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
