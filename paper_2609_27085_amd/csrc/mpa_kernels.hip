@@ -92,6 +92,11 @@ __device__ inline void global_to_lds16(const void* base, unsigned voff, void* ld
   const unsigned off = (unsigned)(size_t)(__attribute__((address_space(3))) void*)lds;
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "s"(off) : "memory");
 }
+// The same copy as a non-temporal (streaming) load, for data read once.
+__device__ inline void global_to_lds16_nt(const void* base, unsigned voff, void* lds) {
+  const unsigned off = (unsigned)(size_t)(__attribute__((address_space(3))) void*)lds;
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1 nt" ::"v"(voff), "s"(base), "s"(off) : "memory");
+}
 
 // Cache reads on the decode path take non-temporal loads: a decode step
 // reads each (block, KV head) granule of K and V once, and marking the loads
@@ -239,19 +244,19 @@ struct Tr<2> {
     return hi ? __builtin_bit_cast(unsigned, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w, 1.0f, true))
               : __builtin_bit_cast(unsigned, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w, 1.0f, false));
   }
-  static __device__ inline Chunk load_chunk(const Elem* p) {
-    const u32x2 w = ld_stream<u32x2>(p);
+  static __device__ inline Chunk k_from_codes(u32x2 w) {
     const u32x4 r = {cvt2(w[0], false), cvt2(w[0], true), cvt2(w[1], false), cvt2(w[1], true)};
     return __builtin_bit_cast(Chunk, r);
   }
-  static __device__ inline Chunk load_q(const QElem* p) { return Tr<0>::load_q(p); }
-  static __device__ inline Chunk zero_chunk() { return Tr<0>::zero_chunk(); }
-  static __device__ inline f32x4 qk(Chunk k, Chunk q, f32x4 c) { return Tr<0>::qk(k, q, c); }
-  static __device__ inline VFrag load_v(const Elem* p) {
-    const unsigned w = ld_stream<unsigned>(p);
+  static __device__ inline VFrag v_from_codes(unsigned w) {
     const u32x2 r = {cvt2(w, false), cvt2(w, true)};
     return __builtin_bit_cast(VFrag, r);
   }
+  static __device__ inline Chunk load_chunk(const Elem* p) { return k_from_codes(ld_stream<u32x2>(p)); }
+  static __device__ inline Chunk load_q(const QElem* p) { return Tr<0>::load_q(p); }
+  static __device__ inline Chunk zero_chunk() { return Tr<0>::zero_chunk(); }
+  static __device__ inline f32x4 qk(Chunk k, Chunk q, f32x4 c) { return Tr<0>::qk(k, q, c); }
+  static __device__ inline VFrag load_v(const Elem* p) { return v_from_codes(ld_stream<unsigned>(p)); }
   static __device__ inline VFrag keep_first(VFrag v, int nvalid) { return Tr<0>::keep_first(v, nvalid); }
   static __device__ inline PFrag make_p(f32x4 p) { return Tr<0>::make_p(p); }
   static __device__ inline PFrag make_p_lo(f32x4 p, PFrag hi) { return Tr<0>::make_p_lo(p, hi); }
@@ -437,6 +442,76 @@ __device__ inline void attend_blocks(const AttnArgs& a, const typename Tr<DT>::C
   }
 }
 
+// attend_blocks for fp8 caches.  A block's K and V granules of one head are
+// 16 * D bytes each; read into registers in the MFMA operand layout they take
+// 8-byte (K) and 4-byte (V) loads per lane, and such narrow loads stream
+// about a tenth slower than 16-byte ones from scattered granules.  So each
+// wave copies whole granules into a private ring of three LDS slots with
+// 16-byte direct-to-LDS loads (non-temporal, 1 KB per instruction), two
+// blocks ahead of the one it consumes, and reads the codes from LDS in the
+// operand layout (conflict-free: a wave's K read covers 512 contiguous
+// bytes, its V read 256).  `ring` is the wave's 3 * 2 * 16 * D bytes of LDS.
+// The copies are counted in vmcnt only (the compiler does not see them), so
+// the waits are explicit; the loop issues no other vector-memory operation.
+template <int D>
+__device__ inline void attend_blocks_fp8_lds(const AttnArgs& a, const bf16x8* qf, const int32_t* bt, int g,
+                                             int kb_begin, int kb_end, int kend, int limit, int min_limit,
+                                             RowState<2, D>& st, bool& poison, uint8_t* ring) {
+  using T = Tr<2>;
+  constexpr int GB = kBlock * D;    // bytes of one granule (K or V of one block and head)
+  constexpr int NI = GB / 1024;     // 1 KB copies per granule
+  constexpr int SLOT = 2 * GB;      // K granule, then V granule
+  constexpr int R = D / (4 * T::X);
+  constexpr int MT = D / 16;
+  static_assert(GB % 1024 == 0, "whole 1 KB copies");
+  const int lane = threadIdx.x & 63;
+  const int n = lane & 15, grp = lane >> 4;
+  const bool few_keys = kend <= kFewKeys;
+  for (int c0 = kb_begin; c0 < kb_end; c0 += 64) {
+    const int c1 = min(kb_end, c0 + 64);
+    const int ids = c0 + lane < c1 ? bt[c0 + lane] : 0;
+    auto block_id = [&](int kb) -> int {
+      int blk = __builtin_amdgcn_readlane(ids, min(kb, c1 - 1) - c0);
+      if (blk < 0 || blk >= a.nb) {
+        poison = true;
+        blk = 0;
+      }
+      return blk;
+    };
+    auto copy = [&](int kb, int slot) {
+      const size_t gran = ((size_t)block_id(kb) * a.hkv + g) * GB;
+      const uint8_t* kp = reinterpret_cast<const uint8_t*>(a.k_cache) + gran;
+      const uint8_t* vp = reinterpret_cast<const uint8_t*>(a.v_cache) + gran;
+#pragma unroll
+      for (int u = 0; u < NI; ++u) {
+        global_to_lds16_nt(kp, (unsigned)(u * 1024 + lane * 16), ring + slot * SLOT + u * 1024);
+        global_to_lds16_nt(vp, (unsigned)(u * 1024 + lane * 16), ring + slot * SLOT + GB + u * 1024);
+      }
+    };
+    copy(c0, 0);
+    copy(c0 + 1, 1);  // past the chunk's last block: that block again (unused)
+    int slot = 0;
+    for (int kb = c0; kb < c1; ++kb) {
+      copy(kb + 2, slot == 0 ? 2 : slot - 1);
+      MPA_WAIT_VMCNT(4 * NI);  // the copies of blocks kb+1 and kb+2 may still be in flight
+      const uint8_t* sp = ring + slot * SLOT;
+      BlockFrags<2, D> f;
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+        f.k[r] = T::k_from_codes(*reinterpret_cast<const u32x2*>(sp + ((4 * r + grp) * kBlock + n) * T::X));
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+        f.v[mt] = T::v_from_codes(*reinterpret_cast<const unsigned*>(sp + GB + (16 * mt + n) * kBlock + 4 * grp));
+      const bool edge = kb * kBlock + kBlock > kend || kb * kBlock + kBlock - 1 > min_limit;
+      consume_block<2, D>(a, qf, f, kb, kend, limit, edge, few_keys, st);
+      slot = slot == 2 ? 0 : slot + 1;
+    }
+    // The ring is reused by the next group of blocks (and the wave's LDS is
+    // released when it ends): no copy may still be writing it.
+    MPA_WAIT_VMCNT(0);
+  }
+}
+
 template <int D>
 __device__ inline void store_fp8_chunk(const AppendArgs& a, size_t head, int c, int slot, u32x4 kw, u32x4 vw);
 
@@ -526,8 +601,14 @@ __global__ __launch_bounds__(256) void decode_kernel(AttnArgs a, DecodePlan p) {
   st.m = -INFINITY;
   st.l = 0.f;
   bool poison = false;
-  attend_blocks<DT, D>(a, qf, a.block_tables + (size_t)s * a.mb, g, k0 / kBlock,
-                       (k1 + kBlock - 1) / kBlock, k1, INT32_MAX, INT32_MAX, st, poison);
+  if constexpr (DT == 2) {
+    __shared__ __attribute__((aligned(16))) uint8_t ring[kWavesPerGroup][3 * 2 * kBlock * D];
+    attend_blocks_fp8_lds<D>(a, qf, a.block_tables + (size_t)s * a.mb, g, k0 / kBlock, (k1 + kBlock - 1) / kBlock,
+                             k1, INT32_MAX, INT32_MAX, st, poison, ring[wave]);
+  } else {
+    attend_blocks<DT, D>(a, qf, a.block_tables + (size_t)s * a.mb, g, k0 / kBlock, (k1 + kBlock - 1) / kBlock, k1,
+                         INT32_MAX, INT32_MAX, st, poison);
+  }
 
   float l = st.l + __shfl_xor(st.l, 16);
   l += __shfl_xor(l, 32);
