@@ -1620,7 +1620,8 @@ hipError_t launch_prefill_mfma(const AttnArgs& a, const PrefillPlan& p, int n_ti
   return hipGetLastError();
 }
 
-// The generic prefill kernel for any dtype (the bf16 few-key pass).
+// Prefill chunks: the MFMA kernel for bf16 and fp8 caches, the generic kernel
+// for f32 ones.
 template <int DT, int D>
 struct PrefillL {
   static hipError_t run(const AttnArgs& a, const PrefillPlan& p, int n_tiles, hipStream_t stream) {
