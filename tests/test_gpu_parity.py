@@ -190,6 +190,33 @@ def test_few_key_rows_at_rounding_floor(torch_gpu, seed, dtype):
     assert excess.max() <= 5e-4, f"few-key rows: {excess.max():.3g} above the bf16 rounding of the exact result"
 
 
+FEW_KEY_SHAPES = [(32, 8, 128), (8, 8, 64), (64, 8, 128), (12, 4, 64)]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+@pytest.mark.parametrize("heads", FEW_KEY_SHAPES, ids=lambda h: f"hq{h[0]}_hkv{h[1]}_d{h[2]}")
+def test_few_key_rows_in_longer_chunks(torch_gpu, heads, dtype):
+    """The same bar for chunks longer than 64 tokens on prefixes of 0 to 64
+    tokens, at group sizes 1, 3, 4 and 8: only the waves of a chunk's first
+    key tile whose rows see at most 64 keys take the second pass, which
+    depends on how many tokens a wave's 32 rows cover; every other row is
+    checked at the usual bars by check_batch."""
+    rng = np.random.default_rng(740 + heads[0])
+    specs = [SeqSpec(p + c, c) for p, c in ((0, 200), (17, 90), (40, 300), (63, 70), (64, 100), (5, 33))]
+    specs += [SeqSpec(int(c), 1) for c in rng.integers(2, 70, size=6)]
+    specs = [specs[i] for i in rng.permutation(len(specs))]
+    b = make_batch(specs, HeadSpec(*heads), dtype, rng)
+    d, out, _ = check_batch(b, f"few-key rows in longer chunks {heads} {dtype}")
+    o_ref, _ = oracle_for(b)
+    keys = np.concatenate([b.seq_lens[s] - b.q_lens[s] + 1 + np.arange(b.q_lens[s]) for s in range(b.num_seqs)])
+    few = keys <= 48
+    assert few.sum() > 0
+    exact = o_ref[few]
+    rounded = bf16_to_f32(bf16_bits_from_f32(exact.astype(np.float32))).astype(np.float64)
+    excess = np.abs(as_f64(out)[few] - exact) - np.abs(rounded - exact)
+    assert excess.max() <= 5e-4, f"few-key rows: {excess.max():.3g} above the bf16 rounding of the exact result"
+
+
 def rope_table(max_pos, rope_dim, base=10000.0):
     j = np.arange(rope_dim // 2)
     ang = np.arange(max_pos)[:, None] * base ** (-2.0 * j / rope_dim)[None, :]
