@@ -1129,34 +1129,88 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
             if (key > limit) st[rt][r] = -INFINITY;
           }
       }
-      // row maximum: four independent chains, then across the two lane halves
-      float m4[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+      // The reference maximum m_ref moves only when some score of the wave
+      // exceeds it by more than thresh (probabilities stay <= 2^8).  On a
+      // wave's first tile it is still -inf and is taken from the tile's row
+      // maximum; on later tiles the probabilities are formed with the current
+      // reference first, and since a score past the threshold makes its
+      // probability -- and so this lane's row-sum partial -- at least 2^8
+      // after bf16 rounding, the tile's maximum is taken only when some
+      // lane's partial reaches 2^8.  Then S is recomputed from the operands
+      // still in LDS (the same products in the same order, so the same
+      // values), the reference is moved if the threshold is passed, and the
+      // probabilities are formed again.  Either way the probabilities, the
+      // row sums and the reference are those of taking the maximum on every
+      // tile.
+      auto row_max = [&](const f32x16 (&s)[2]) -> float {
+        float m4[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt)
+        for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) m4[r & 3] = fmaxf(m4[r & 3], st[rt][r]);
-      const float mx = max_across_halves(fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3])));
-      if (__any(mx > m_ref + thresh)) {
+          for (int r = 0; r < 16; ++r) m4[r & 3] = fmaxf(m4[r & 3], s[rt][r]);
+        return max_across_halves(fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3])));
+      };
+      auto move_reference = [&](float mx) {
         const float m_new = fmaxf(m_ref, mx);
         const float alpha = m_new == -INFINITY ? 1.f : exp2_fast((m_ref - m_new) * c);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
         l *= alpha;
         m_ref = m_new;
-      }
-      const float mc = m_ref * c;
+      };
       // P^T in bf16; the row sum adds the rounded values the PV product
       // uses (four independent partial sums, two probabilities per dot2).
       bf16x8 pb[4];
-      float l4[4] = {0.f, 0.f, 0.f, 0.f};
+      float l4[4];
+      auto make_p = [&](const f32x16 (&s)[2], float mc) {
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
+        for (int k = 0; k < 4; ++k) l4[k] = 0.f;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) pb[t][e] = (__bf16)exp2_fast(fmaf(st[t >> 1][8 * (t & 1) + e], c, -mc));
-        const u32x4 w = __builtin_bit_cast(u32x4, pb[t]);
+        for (int t = 0; t < 4; ++t) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) l4[k] = add_bf16_pair(w[k], l4[k]);
+          for (int e = 0; e < 8; ++e) pb[t][e] = (__bf16)exp2_fast(fmaf(s[t >> 1][8 * (t & 1) + e], c, -mc));
+          const u32x4 w = __builtin_bit_cast(u32x4, pb[t]);
+#pragma unroll
+          for (int k = 0; k < 4; ++k) l4[k] = add_bf16_pair(w[k], l4[k]);
+        }
+      };
+      if (kt == kt_begin) {
+        const float mx = row_max(st);
+        if (__any(mx > m_ref + thresh)) move_reference(mx);
       }
+      make_p(st, m_ref * c);
+      if (kt != kt_begin && __any(!((l4[0] + l4[1]) + (l4[2] + l4[3]) < 256.f))) {
+        asm volatile("" ::: "memory");
+        f32x16 s2[2];
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) s2[rt][r] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+          for (int rt = 0; rt < 2; ++rt)
+            s2[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8,
+                                   *reinterpret_cast<const u32x4*>(K + 2 * rt * BLK + koff + (2 * ks + h) * 128)),
+                qf[ks], s2[rt], 0, 0, 0);
+        if (key_base + BN - 1 > w_min_limit) {
+#pragma unroll
+          for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int jr = r >> 2;
+              const int key = key_base + 32 * rt + 16 * (jr >> 1) + 8 * h + 4 * (jr & 1) + (r & 3);
+              if (key > limit) s2[rt][r] = -INFINITY;
+            }
+        }
+        const float mx = row_max(s2);
+        if (__any(mx > m_ref + thresh)) {
+          move_reference(mx);
+          make_p(s2, m_ref * c);
+        }
+      }
+      const float mc = m_ref * c;
 #pragma unroll
       for (int t = 0; t < 4; ++t)
 #pragma unroll

@@ -21,6 +21,7 @@ import pytest
 import paper_2609_27085_amd as mpa
 from oracle import ref
 from workloads import HeadSpec, SeqSpec, bf16_bits_from_f32, make_batch
+from workloads.gen import _fp8_nearest_codes
 from workloads.configs import config_batch, config_specs
 from workloads.device import device_step, host_subbatch, tensor_to_raw, to_device
 
@@ -215,6 +216,64 @@ def test_few_key_rows_in_longer_chunks(torch_gpu, heads, dtype):
     rounded = bf16_to_f32(bf16_bits_from_f32(exact.astype(np.float32))).astype(np.float64)
     excess = np.abs(as_f64(out)[few] - exact) - np.abs(rounded - exact)
     assert excess.max() <= 5e-4, f"few-key rows: {excess.max():.3g} above the bf16 rounding of the exact result"
+
+
+def _cache_floats(raw, dtype, scale):
+    """bf16 bit patterns or E4M3 codes (times the cache scale) as float64."""
+    if dtype == "bf16":
+        return bf16_to_f32(raw).astype(np.float64)
+    c = raw.astype(np.int64)
+    e, m = (c >> 3) & 15, c & 7
+    v = np.where(e == 0, m * 2.0 ** -9, (1 + m / 8.0) * 2.0 ** (e - 7.0))
+    return np.where(c & 0x80, -v, v) * scale
+
+
+def _cache_raw(x, dtype, scale):
+    return bf16_bits_from_f32(x.astype(np.float32)) if dtype == "bf16" else _fp8_nearest_codes(x / scale)
+
+
+@pytest.mark.parametrize("splits", ["1", "auto"])
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_reference_moves_in_later_tiles(torch_gpu, dtype, splits, monkeypatch):
+    """Scores that keep rising along the cached prefix, so that a chunk row's
+    reference maximum moves on tiles after its first one (and row-sum
+    partials reach 2^8 between moves): the chunks' queries share a component
+    256 u, and each cached key has its u component replaced by a ramp that
+    adds 0.03 to the scaled score per position (the rest of the key scaled
+    by 1/4, so that some 30 keys near the top weigh alike and the bf16
+    rounding of P averages as usual).  The rows climb by more than 128 log2 units
+    over the longer prefixes, so a reference that did not move would
+    overflow the probabilities.  With and without prefix KV splits (a
+    split's first tile takes the full row maximum)."""
+    if splits == "1":
+        monkeypatch.setenv("MPA_PREFILL_SPLITS", "1")
+    rng = np.random.default_rng(770)
+    heads = HeadSpec(32, 8, 128)
+    chunks = [(3000, 200), (4000, 64), (3500, 130)]
+    specs = [SeqSpec(p + c, c) for p, c in chunks] + [SeqSpec(int(c), 1) for c in rng.integers(100, 900, size=3)]
+    b = make_batch(specs, heads, dtype, rng)
+    d = heads.head_dim
+    u = rng.standard_normal(d)
+    u /= np.linalg.norm(u)
+    gamma = 256.0
+    climbs = []
+    for i, (p, c) in enumerate(chunks):
+        t0 = b.query_start_loc[i]
+        q = bf16_to_f32(b.q[t0:t0 + c]).astype(np.float64) + gamma * u
+        b.q[t0:t0 + c] = bf16_bits_from_f32(q.astype(np.float32))
+        pos = np.arange(p)
+        blk, slot = b.block_tables[i, pos // 16], pos % 16
+        ramp = 0.03 * pos / (gamma * b.scale)
+        for g in range(heads.num_kv_heads):
+            k = _cache_floats(b.k_cache[blk, g, :, slot, :], dtype, b.k_scale).reshape(p, d)
+            k = 0.25 * (k - np.outer(k @ u, u)) + np.outer(ramp, u)
+            b.k_cache[blk, g, :, slot, :] = _cache_raw(k, dtype, b.k_scale).reshape(p, d // b.k_cache.shape[-1], -1)
+        # how far the first row's scores (head 0) climb past the first tile
+        k0 = _cache_floats(b.k_cache[blk, 0, :, slot, :], dtype, b.k_scale).reshape(p, d)
+        s0 = (k0 @ bf16_to_f32(b.q[t0, 0]).astype(np.float64)) * b.scale / np.log(2.0)
+        climbs.append(s0[64:].max() - s0[:64].max())
+    assert min(climbs) > 16.0 and max(climbs) > 140.0, climbs
+    check_batch(b, f"reference moving in later tiles {dtype} splits={splits}")
 
 
 def rope_table(max_pos, rope_dim, base=10000.0):
