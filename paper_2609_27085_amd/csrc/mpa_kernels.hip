@@ -944,7 +944,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   // every copy is issued, always 2*WI instructions per wave per tile.
   // the id of the block this wave copies for tile kt (a scalar load)
   auto tile_block = [&](int kt) -> int { return bt[min(kt * NB + my_bi, nblk - 1)]; };
-  auto copy_tile = [&](int kt, int blk_raw) -> int {
+  auto copy_tile = [&](int blk_raw, int stage) -> int {
     const int blk = (blk_raw >= 0 && blk_raw < a.nb) ? blk_raw : 0;
     if constexpr (CT == 2) {
       if (pi < NB * D) {
@@ -952,10 +952,9 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
         kraw = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint8_t*>(a.k_cache) + gran);
         vraw = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint8_t*>(a.v_cache) + gran);
       }
-      (void)kt;
+      (void)stage;
       return blk_raw;
     }
-    const int stage = kt % STAGES;
     const size_t gran = ((size_t)blk * a.hkv + g) * BLK;
     const uint16_t* kbase = reinterpret_cast<const uint16_t*>(a.k_cache) + gran;
     const uint16_t* vbase = reinterpret_cast<const uint16_t*>(a.v_cache) + gran;
@@ -976,11 +975,10 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   // After this wave's copy of tile kt has landed: zero its V entries of keys
   // >= L (the tail of the sequence's last block, and clamped blocks), or fill
   // them with NaN when the block id was invalid.
-  auto fix_tile = [&](int kt, int blk_raw) {
+  auto fix_tile = [&](int kt, int blk_raw, int stage) {
     const int nvalid_blk = L - (kt * NB + my_bi) * kBlock;
     const bool bad = !(blk_raw >= 0 && blk_raw < a.nb);
     if (!bad && nvalid_blk >= kBlock) return;
-    const int stage = kt % STAGES;
 #pragma unroll
     for (int u = 0; u < WI; ++u) {
       const int ii = wave * WI + u;
@@ -997,11 +995,11 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   // in the tile's stage -- K piece q (keys 2j, 2j+1 of chunk c = q/8, j = q%8)
   // at the slots of those keys, V piece q (V^T row q, 16 keys) as its two key
   // halves -- with the V entries of keys >= L zeroed (NaN for a bad block id)
-  auto store_fp8_tile = [&](int kt, int blk_raw) {
+  auto store_fp8_tile = [&](int kt, int blk_raw, int stage) {
     if (pi >= NB * D) return;
     const int b = pi / D, q = pi % D;
-    uint8_t* kdst = reinterpret_cast<uint8_t*>(sk + (kt % STAGES) * TILE + b * BLK);
-    uint8_t* vdst = reinterpret_cast<uint8_t*>(sv + (kt % STAGES) * TILE + b * BLK);
+    uint8_t* kdst = reinterpret_cast<uint8_t*>(sk + stage * TILE + b * BLK);
+    uint8_t* vdst = reinterpret_cast<uint8_t*>(sv + stage * TILE + b * BLK);
     const int c = q >> 3, j = q & 7;
 #pragma unroll
     for (int x = 0; x < 2; ++x) {
@@ -1046,19 +1044,27 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   // the Q fragments (ordinary loads) land before any tile copy is issued, so
   // that no wait inside the loop is ever needed for them
   MPA_WAIT_VMCNT(0);
+  // Stages rotate: tile kt sits in stage kt % STAGES, kept as counters that
+  // step each iteration (s_use for tile kt, s_next for kt+1, s_copy for
+  // kt+AHEAD).  The block ids of the tiles copied but not yet fixed up wait
+  // in ids[]: ids[0] is tile kt+1's, ids[AHEAD-1] tile kt+AHEAD's.
+  auto wrap = [](int x) { return x >= STAGES ? x - STAGES : x; };
+  int s_use = kt_begin % STAGES;
+  int ids[AHEAD];
   // prologue: the split's first AHEAD tiles in flight, its first published
-  int blk_id[STAGES];
 #pragma unroll
-  for (int k = 0; k < AHEAD; ++k) blk_id[(kt_begin + k) % STAGES] = copy_tile(kt_begin + k, tile_block(kt_begin + k));
+  for (int k = 0; k < AHEAD; ++k) ids[k] = copy_tile(tile_block(kt_begin + k), wrap(s_use + k));
   // each iteration loads the block id the next one copies (see below)
   int next_blk = tile_block(kt_begin + AHEAD);
   if constexpr (CT == 2) {
     MPA_WAIT_VMCNT(0);
-    store_fp8_tile(kt_begin, blk_id[kt_begin % STAGES]);
+    store_fp8_tile(kt_begin, ids[0], s_use);
   } else {
     MPA_WAIT_VMCNT(2 * WI * (STAGES - 2));
-    fix_tile(kt_begin, blk_id[kt_begin % STAGES]);
+    fix_tile(kt_begin, ids[0], s_use);
   }
+#pragma unroll
+  for (int k = 0; k + 1 < AHEAD; ++k) ids[k] = ids[k + 1];
   __syncthreads();
 
   // Waves w and w + WAVES/2 share a SIMD and run the same phases; the issue
@@ -1071,11 +1077,12 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
     // past it): by an active wave between its first QK products, so that the
     // copy instructions are issued while the matrix core is busy
     const int cblk = next_blk;
-    blk_id[(kt + AHEAD) % STAGES] = cblk;
+    ids[AHEAD - 1] = cblk;
+    const int s_next = wrap(s_use + 1), s_copy = wrap(s_use + AHEAD);
     const int key_base = kt * BN;
     if (wave_active && key_base < w_kend) {
-      const uint16_t* K = sk + (kt % STAGES) * TILE;
-      const uint16_t* V = sv + (kt % STAGES) * TILE;
+      const uint16_t* K = sk + s_use * TILE;
+      const uint16_t* V = sv + s_use * TILE;
       // All K operands of the tile are read from LDS before the first MFMA,
       // so the reads' latency overlaps instead of separating every MFMA pair
       // (left to itself the scheduler reuses one register quad for them all).
@@ -1101,7 +1108,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
           st[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[rt][ks], qf[ks], st[rt], 0, 0, 0);
         if (ks == 1) {
           __builtin_amdgcn_sched_barrier(0);
-          copy_tile(kt + AHEAD, cblk);
+          copy_tile(cblk, s_copy);
           __builtin_amdgcn_sched_barrier(0);
         }
       }
@@ -1269,7 +1276,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
         l += (r4[0] + r4[1]) + (r4[2] + r4[3]);
       }
     } else {
-      copy_tile(kt + AHEAD, cblk);
+      copy_tile(cblk, s_copy);
       next_blk = tile_block(kt + AHEAD + 1);
       // The block id is a scalar load, which shares the LDS counter and may
       // return out of order.  Left pending on this path, it would reach the
@@ -1280,13 +1287,16 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
     if constexpr (CT == 2) {
       // this lane's pieces of tile kt+1 (the only loads in flight)
       MPA_WAIT_VMCNT(0);
-      store_fp8_tile(kt + 1, blk_id[(kt + 1) % STAGES]);
+      store_fp8_tile(kt + 1, ids[0], s_next);
     } else {
       // this wave's part of tile kt+1 has landed once only the copies issued
       // after it (tiles kt+2 .. kt+STAGES-1) remain in flight
       MPA_WAIT_VMCNT(2 * WI * (STAGES - 2));
-      fix_tile(kt + 1, blk_id[(kt + 1) % STAGES]);
+      fix_tile(kt + 1, ids[0], s_next);
     }
+#pragma unroll
+    for (int k = 0; k + 1 < AHEAD; ++k) ids[k] = ids[k + 1];
+    s_use = s_next;
     __syncthreads();
   }
   MPA_WAIT_VMCNT(0);  // drain the clamped copies past the end
