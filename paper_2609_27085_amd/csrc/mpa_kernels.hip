@@ -944,8 +944,13 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   // every copy is issued, always 2*WI instructions per wave per tile.
   // the id of the block this wave copies for tile kt (a scalar load)
   auto tile_block = [&](int kt) -> int { return bt[min(kt * NB + my_bi, nblk - 1)]; };
+  // Byte offsets of the bf16 granules: consecutive cache blocks are
+  // blk_bytes apart, this KV head's granule head_bytes into its block (both
+  // below 2^32 for any head count the shape check admits).
+  const unsigned blk_bytes = (unsigned)a.hkv * (unsigned)(BLK * 2);
+  const unsigned head_bytes = (unsigned)g * (unsigned)(BLK * 2);
   auto copy_tile = [&](int blk_raw, int stage) -> int {
-    const int blk = (blk_raw >= 0 && blk_raw < a.nb) ? blk_raw : 0;
+    const unsigned blk = (unsigned)blk_raw < (unsigned)a.nb ? (unsigned)blk_raw : 0u;
     if constexpr (CT == 2) {
       if (pi < NB * D) {
         const size_t gran = ((size_t)blk * a.hkv + g) * (kBlock * D) + (size_t)(pi % D) * 16;
@@ -955,9 +960,9 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
       (void)stage;
       return blk_raw;
     }
-    const size_t gran = ((size_t)blk * a.hkv + g) * BLK;
-    const uint16_t* kbase = reinterpret_cast<const uint16_t*>(a.k_cache) + gran;
-    const uint16_t* vbase = reinterpret_cast<const uint16_t*>(a.v_cache) + gran;
+    const uint64_t gran = (uint64_t)blk * blk_bytes + head_bytes;
+    const uint8_t* kbase = reinterpret_cast<const uint8_t*>(a.k_cache) + gran;
+    const uint8_t* vbase = reinterpret_cast<const uint8_t*>(a.v_cache) + gran;
 #pragma unroll
     for (int u = 0; u < WI; ++u) {
       const int ii = wave * WI + u;                 // 1 KB slice of the tile
@@ -975,10 +980,13 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   // After this wave's copy of tile kt has landed: zero its V entries of keys
   // >= L (the tail of the sequence's last block, and clamped blocks), or fill
   // them with NaN when the block id was invalid.
+  // the first tile whose block copied by this wave holds keys >= L
+  const int nfull = L / kBlock;
+  const int kt_fix_from = nfull <= my_bi ? 0 : (nfull - my_bi + NB - 1) / NB;
   auto fix_tile = [&](int kt, int blk_raw, int stage) {
+    const bool bad = (unsigned)blk_raw >= (unsigned)a.nb;
+    if (kt < kt_fix_from && !bad) return;
     const int nvalid_blk = L - (kt * NB + my_bi) * kBlock;
-    const bool bad = !(blk_raw >= 0 && blk_raw < a.nb);
-    if (!bad && nvalid_blk >= kBlock) return;
 #pragma unroll
     for (int u = 0; u < WI; ++u) {
       const int ii = wave * WI + u;
