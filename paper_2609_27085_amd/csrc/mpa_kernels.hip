@@ -869,6 +869,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   constexpr int BLK = kBlock * D;          // elements of one (block, head) granule
   constexpr int TILE = NB * BLK;           // elements of one K (or V) tile
   constexpr int KS = D / 16;               // k-steps of the QK^T product
+  static_assert(KS >= 4, "the V reads follow the last four k-steps");
   constexpr int DT = D / 32;               // 32-dim row tiles of O^T
   constexpr int NI = TILE * 2 / 1024;      // 1 KB copies per tile and cache
   constexpr int WI = NI / WAVES;           // ... per wave
@@ -1107,6 +1108,12 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
       for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) st[rt][r] = 0.f;
+      // V operands: the reads of cache block t of the tile are issued after
+      // k-step KS-4+t of the QK product, into registers whose K operands
+      // that step has consumed.  Spread over the last four k-steps, the
+      // eight waves' V reads do not all reach the LDS at once when the
+      // products end, and they land while the softmax runs.
+      bf16x8 vf[4][DT];
       // the two 32-key row tiles are independent accumulation chains:
       // interleave them so back-to-back MFMAs never wait on each other
 #pragma unroll
@@ -1114,21 +1121,21 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
           st[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[rt][ks], qf[ks], st[rt], 0, 0, 0);
-        if (ks == 1) {
+        if (ks == 2) {
           __builtin_amdgcn_sched_barrier(0);
           copy_tile(cblk, s_copy);
           __builtin_amdgcn_sched_barrier(0);
         }
+        if (ks >= KS - 4) {
+          const int t = ks - (KS - 4);
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+            vf[t][dt] = __builtin_bit_cast(
+                bf16x8, *reinterpret_cast<const u32x4*>(V + t * BLK + (h * D + n) * 8 + 32 * dt * 8));
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
-      // V operands: issued now, they land while the softmax runs
-      bf16x8 vf[4][DT];
-#pragma unroll
-      for (int t = 0; t < 4; ++t)
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-          vf[t][dt] = __builtin_bit_cast(
-              bf16x8, *reinterpret_cast<const u32x4*>(V + t * BLK + (h * D + n) * 8 + 32 * dt * 8));
-      __builtin_amdgcn_sched_barrier(0);
       // the next copy's block id: a scalar load shares the LDS wait counter
       // and may complete out of order, so issued here, after the last LDS
       // read of the tile, it only turns the PV waits into full ones, by
