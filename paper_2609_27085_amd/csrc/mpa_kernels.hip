@@ -1092,16 +1092,22 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
     if (wave_active && key_base < w_kend) {
       const uint16_t* K = sk + s_use * TILE;
       const uint16_t* V = sv + s_use * TILE;
-      // All K operands of the tile are read from LDS before the first MFMA,
-      // so the reads' latency overlaps instead of separating every MFMA pair
-      // (left to itself the scheduler reuses one register quad for them all).
+      // The K operands of the first KUP k-steps are read from LDS before the
+      // first MFMA, and each later k-step's KUP steps ahead of its use, each
+      // into registers of its own: the reads' latency overlaps instead of
+      // separating every MFMA pair (left to itself the scheduler reuses one
+      // register quad for them all), and the eight waves do not queue all
+      // of the tile's K reads at the LDS at once when the tile is published.
+      constexpr int KUP = 3;
       bf16x8 kf[2][KS];
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
+      auto read_k = [&](int ks) {
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
           kf[rt][ks] =
               __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(K + 2 * rt * BLK + koff + (2 * ks + h) * 128));
+      };
+#pragma unroll
+      for (int ks = 0; ks < KUP; ++ks) read_k(ks);
       __builtin_amdgcn_sched_barrier(0);
       f32x16 st[2];
 #pragma unroll
@@ -1121,6 +1127,11 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
           st[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[rt][ks], qf[ks], st[rt], 0, 0, 0);
+        if (ks + KUP < KS) {
+          __builtin_amdgcn_sched_barrier(0);
+          read_k(ks + KUP);
+          __builtin_amdgcn_sched_barrier(0);
+        }
         if (ks == 2) {
           __builtin_amdgcn_sched_barrier(0);
           copy_tile(cblk, s_copy);
