@@ -569,8 +569,12 @@ void mpa_default_rates(mpa_rates* r) {
   r->decode_gbs = 5880.0;
   r->decode_wave_gbs = 4.8;
   r->merge_us = 5.0;
-  r->prefill_wg_us = 18.0;
-  r->prefill_tile_us = 1.85;
+  // prefill: refitted to the prefill half alone (lent, agentic, the budget
+  // chunks, longctx) on two devices whose prefill rates differ by 5-7 %,
+  // the mean of the two least-squares fits (12 + 1.80 per tile and 11.9 +
+  // 1.76 against 12.1 + 1.85)
+  r->prefill_wg_us = 12.0;
+  r->prefill_tile_us = 1.80;
   r->prefill_merge_us = 3.0;
   r->prefill_merge_row_us = 1.6e-4;
   // A partitioned step's fixed cost beyond the model (the cross-stream waits,
