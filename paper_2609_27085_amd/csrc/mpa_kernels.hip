@@ -950,13 +950,14 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   // below 2^32 for any head count the shape check admits).
   const unsigned blk_bytes = (unsigned)a.hkv * (unsigned)(BLK * 2);
   const unsigned head_bytes = (unsigned)g * (unsigned)(BLK * 2);
-  auto copy_tile = [&](int blk_raw, int stage) -> int {
+  // which: 1 the K slices, 2 the V slices, 3 both
+  auto copy_tile = [&](int blk_raw, int stage, int which = 3) -> int {
     const unsigned blk = (unsigned)blk_raw < (unsigned)a.nb ? (unsigned)blk_raw : 0u;
     if constexpr (CT == 2) {
       if (pi < NB * D) {
         const size_t gran = ((size_t)blk * a.hkv + g) * (kBlock * D) + (size_t)(pi % D) * 16;
-        kraw = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint8_t*>(a.k_cache) + gran);
-        vraw = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint8_t*>(a.v_cache) + gran);
+        if (which & 1) kraw = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint8_t*>(a.k_cache) + gran);
+        if (which & 2) vraw = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint8_t*>(a.v_cache) + gran);
       }
       (void)stage;
       return blk_raw;
@@ -971,10 +972,10 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
       // K: piece (chunk c, slot) <- key swap23(slot) of chunk c
       const int kc = cq >> 4, ks16 = cq & 15;
       const int kkey = (ks16 & 3) | ((ks16 & 4) << 1) | ((ks16 & 8) >> 1);
-      global_to_lds16(kbase, (unsigned)((kc * 16 + kkey) * 16), sk + stage * TILE + ii * 512);
+      if (which & 1) global_to_lds16(kbase, (unsigned)((kc * 16 + kkey) * 16), sk + stage * TILE + ii * 512);
       // V: piece (half vh, row d) <- keys 8vh..8vh+7 of V^T row d
       const int vh = cq / D, vd = cq % D;
-      global_to_lds16(vbase, (unsigned)((vd * kBlock + vh * 8) * 2), sv + stage * TILE + ii * 512);
+      if (which & 2) global_to_lds16(vbase, (unsigned)((vd * kBlock + vh * 8) * 2), sv + stage * TILE + ii * 512);
     }
     return blk_raw;
   };
@@ -1083,7 +1084,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
   if (wave >= WAVES / 2) __builtin_amdgcn_s_setprio(1);
   for (int kt = kt_begin; kt < ntile; ++kt) {
     // tile kt+STAGES-1 is copied into the stage tile kt-1 used (all waves are
-    // past it): by an active wave between its first QK products, so that the
+    // past it): by an active wave between its QK products, so that the
     // copy instructions are issued while the matrix core is busy
     const int cblk = next_blk;
     ids[AHEAD - 1] = cblk;
@@ -1132,9 +1133,14 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
           read_k(ks + KUP);
           __builtin_amdgcn_sched_barrier(0);
         }
-        if (ks == 2) {
+        // the next tile copy: bf16 tiles as their K slices after the third
+        // k-step and their V slices after k-step KS/2 (the same step at
+        // D = 64); fp8 pieces both after the third, since they must land
+        // by the end of this tile
+        constexpr int v_ks = CT == 0 ? KS / 2 : 2;
+        if (ks == 2 || ks == v_ks) {
           __builtin_amdgcn_sched_barrier(0);
-          copy_tile(cblk, s_copy);
+          copy_tile(cblk, s_copy, (ks == 2 ? 1 : 0) | (ks == v_ks ? 2 : 0));
           __builtin_amdgcn_sched_barrier(0);
         }
         if (ks >= KS - 4) {
