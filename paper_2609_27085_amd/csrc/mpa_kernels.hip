@@ -1135,12 +1135,13 @@ __global__ __launch_bounds__(64 * WAVES, 1) void prefill_mfma_kernel(AttnArgs a,
         }
         // the next tile copy: bf16 tiles as their K slices after the third
         // k-step and their V slices after k-step KS/2 (the same step at
-        // D = 64); fp8 pieces both after the third, since they must land
-        // by the end of this tile
-        constexpr int v_ks = CT == 0 ? KS / 2 : 2;
-        if (ks == 2 || ks == v_ks) {
+        // D = 64); fp8 pieces both after the first, since they must land
+        // in registers by the end of this tile
+        constexpr int k_ks = CT == 0 ? 2 : 0;
+        constexpr int v_ks = CT == 0 ? KS / 2 : 0;
+        if (ks == k_ks || ks == v_ks) {
           __builtin_amdgcn_sched_barrier(0);
-          copy_tile(cblk, s_copy, (ks == 2 ? 1 : 0) | (ks == v_ks ? 2 : 0));
+          copy_tile(cblk, s_copy, (ks == k_ks ? 1 : 0) | (ks == v_ks ? 2 : 0));
           __builtin_amdgcn_sched_barrier(0);
         }
         if (ks >= KS - 4) {
