@@ -45,6 +45,28 @@ int check_shape(const mpa_shape* sh) {
   return MPA_OK;
 }
 
+// Whether the planner leaves every prefill chunk of the batch whole (one KV
+// split each): f32 chunks, and MFMA batches with at least two workgroups
+// per CU or no prefix long enough to split, unless MPA_PREFILL_SPLITS
+// overrides the choice.  prefill_splits() takes the same decision.
+bool prefill_whole(const mpa_shape* sh, const std::vector<int>& prefill, const int32_t* seq_lens,
+                   const int32_t* qsl) {
+  if (sh->dtype == MPA_F32 || prefill.empty()) return true;
+  if (const char* env = getenv("MPA_PREFILL_SPLITS")) {
+    const int v = atoi(env);
+    if (v >= 1 && v <= 64) return false;
+  }
+  const int qt = mpa::kPrefillRowsMfma / (sh->num_q_heads / sh->num_kv_heads);
+  long units = 0;
+  int most = 1;  // the most splits any chunk can take
+  for (int s : prefill) {
+    const int C = qsl[s + 1] - qsl[s];
+    units += (long)(C + qt - 1) / qt * sh->num_kv_heads;
+    most = std::max(most, std::min(1 + (seq_lens[s] - C) / 64 / mpa::kPrefillMinSplitTiles, 64));
+  }
+  return units >= 2L * mpa::kPrefillSplitTarget || most == 1;
+}
+
 // Validates the host metadata and classifies the sequences.
 int check_batch(const mpa_shape* sh, const int32_t* seq_lens, const int32_t* qsl, const int32_t* bt_host,
                 bool append_only, Batch* b) {
@@ -76,6 +98,13 @@ int check_batch(const mpa_shape* sh, const int32_t* seq_lens, const int32_t* qsl
       b->prefill.push_back(s);
     }
   }
+  // The MFMA prefill kernel dispatches its work units from the plan's last
+  // chunk backwards, each chunk from its longest query tile (the one that
+  // sees all L keys).  With whole chunks ordered by L, the longest units go
+  // first and the short ones fill the end of the launch.  A split chunk's
+  // units are not ordered by length, so split batches keep batch order.
+  if (sh->dtype != MPA_F32 && b->prefill.size() > 1 && prefill_whole(sh, b->prefill, seq_lens, qsl))
+    std::stable_sort(b->prefill.begin(), b->prefill.end(), [&](int x, int y) { return seq_lens[x] < seq_lens[y]; });
   return MPA_OK;
 }
 
@@ -298,6 +327,7 @@ std::vector<PrefillSplit> prefill_splits(const mpa_shape* sh, const Batch& b, co
     const int v = atoi(env);
     if (v >= 1 && v <= 64) return split_layout(b, seq_lens, qsl, v, first_item);
   }
+  if (prefill_whole(sh, b.prefill, seq_lens, qsl)) return std::vector<PrefillSplit>(b.prefill.size());
   const int qt = q_tile(sh);
   long units = 0;
   int most = 1;  // the most splits any chunk can take
@@ -306,7 +336,6 @@ std::vector<PrefillSplit> prefill_splits(const mpa_shape* sh, const Batch& b, co
     units += (long)(C + qt - 1) / qt * sh->num_kv_heads;
     most = std::max(most, std::min(1 + (seq_lens[s] - C) / 64 / mpa::kPrefillMinSplitTiles, 64));
   }
-  if (units >= 2L * mpa::kPrefillSplitTarget || most == 1) return std::vector<PrefillSplit>(b.prefill.size());
   PlanMemo& m = plan_memo(sh, seq_lens, qsl);
   if (m.want == 0) {
     double best_t = -1.0;
