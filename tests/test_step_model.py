@@ -117,6 +117,27 @@ def test_prefill_makespan_by_hand(L):
     assert predict(chunks=[(64, 0)], rates=r, **kw).prefill_us == pytest.approx(111.0)
 
 
+def test_whole_batch_dispatch_order_ignores_batch_order(L):
+    """A batch the planner leaves whole (here 1,496 work units, agentic-like
+    chunks at 64/8 heads) has its chunks dispatched by length, whatever order
+    the caller lists the sequences in: the predicted prefill time, which walks
+    the launch's own unit order, is the same for every order of the chunks
+    and with decode rows placed anywhere among them."""
+    import itertools
+
+    chunks = [(1667, 14960), (1319, 12080), (2008, 13120), (915, 10576)]
+    kw = dict(hq=64, hkv=8)
+    want = predict([6000, 9000], chunks, **kw).prefill_us
+    assert want > 0.0
+    for perm in itertools.permutations(range(len(chunks))):
+        assert predict([6000, 9000], [chunks[i] for i in perm], **kw).prefill_us == want
+    # decode rows between and after the chunks
+    rows = [(1, 6000)] + [(c, p + c) for c, p in chunks[:2]] + [(1, 9000)] + [(c, p + c) for c, p in chunks[2:]]
+    sl = np.asarray([L_ for _, L_ in rows], np.int32)
+    qsl = np.concatenate([[0], np.cumsum([q for q, _ in rows])]).astype(np.int32)
+    assert mpa.predict_step(shape(sl, qsl, **kw), sl, qsl).prefill_us == want
+
+
 def test_short_chunk_on_long_prefix_is_split(L):
     # 256 tokens on a 4352-token prefix: 4 query tiles x 8 heads = 32 units,
     # so the library splits the prefix 8 ways (see the planner test); the
