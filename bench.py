@@ -14,9 +14,11 @@ before timing starts.  Prints one JSON line:
                  memory (a cache flush) and bracketed by its own two events
                  (--flush-mb 0: wall clock over back-to-back steps)
   roofline       the dominant half's algorithmic bytes (or FLOPs) per launch
-                 over its average duration: --phase-reps back-to-back launches
-                 of that half's attention call alone (no append), between one
-                 event pair on its stream, against the MI355X datasheet peak
+                 over its average duration: back-to-back launches of that
+                 half's attention call alone (no append), at least --phase-reps
+                 and at least 20 ms of them after at least 25 ms of untimed
+                 ones, between one event pair on its stream, against the
+                 MI355X datasheet peak
                  (HBM 8 TB/s, bf16 dense MFMA 2.5 PF)
   decode_hbm_gbs, prefill_tflops
                  the same for each half present
@@ -266,8 +268,9 @@ def main(argv=None) -> int:
                          "step with its own events; value comes from the median step (default 512; 0: back-to-back "
                          "steps, wall clock)")
     ap.add_argument("--phase-reps", type=int, default=10, metavar="N",
-                    help="back-to-back launches of each attention half alone (after two untimed ones), between one "
-                         "event pair on its stream: the phase rates and the roofline (default 10)")
+                    help="at least N back-to-back launches (and at least 20 ms) of each attention half alone, after "
+                         "at least 25 ms of untimed ones, between one event pair on its stream: the phase rates and the "
+                         "roofline (default 10)")
     ap.add_argument("--graph", action="store_true",
                     help="also capture one step into a HIP graph (torch.cuda.graph) and time its replays")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -419,9 +422,14 @@ def main(argv=None) -> int:
         ms_per_step = wall * 1e3 / args.steps
         value = work["query_tokens"] * args.steps / wall
 
-    # Each half's attention call alone (no append): phase_reps launches back
-    # to back between one event pair on the stream they run on (a partition
-    # stream in co-execution mode), after two untimed launches.
+    # Each half's attention call alone (no append): back-to-back launches
+    # between one event pair on the stream they run on (a partition stream in
+    # co-execution mode), at least phase_reps of them and at least 20 ms,
+    # after untimed launches that fill at least 25 ms of device time, so that
+    # a short kernel is timed in the same steady state as a long one (the
+    # first few milliseconds of launches after other work run slower).
+    how_alone = {}
+
     def half_alone_ms(which):
         fn = mpa.decode_attention if which == "decode" else mpa.prefill_attention
         st = torch.cuda.current_stream()
@@ -432,16 +440,26 @@ def main(argv=None) -> int:
             fn(d.q, d.k_cache, d.v_cache, d.block_tables, d.seq_lens, d.query_start_loc, d.seq_lens_host,
                d.qsl_host, out, lse=lse, workspace=ws, scale=d.scale, stream=st, **sc)
 
-        for _ in range(2):
-            launch()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         a.record(st)
-        for _ in range(max(1, args.phase_reps)):
+        for _ in range(2):
             launch()
         b.record(st)
         torch.cuda.synchronize()
-        return a.elapsed_time(b) / max(1, args.phase_reps)
+        per = max(a.elapsed_time(b) / 2, 1e-3)
+        warm = 2 + min(1000, max(0, int(np.ceil((25.0 - 2 * per) / per))))
+        for _ in range(warm - 2):
+            launch()
+        reps = max(1, args.phase_reps, min(2000, int(np.ceil(20.0 / per))))
+        torch.cuda.synchronize()
+        a.record(st)
+        for _ in range(reps):
+            launch()
+        b.record(st)
+        torch.cuda.synchronize()
+        how_alone[which] = (reps, warm)
+        return a.elapsed_time(b) / reps
 
     alone = {}
     if has_dec:
@@ -476,8 +494,8 @@ def main(argv=None) -> int:
         "kernel": kernel,
         "phase_ms": round(dom_ms, 4),
         "algorithmic_per_launch": work["decode_bytes"] if dom == "decode" else work["prefill_flops"],
-        "how": f"{max(1, args.phase_reps)} back-to-back launches of mpa_{dom}_attention alone (no append) between "
-               "one event pair on its stream, after two untimed launches",
+        "how": f"{how_alone[dom][0]} back-to-back launches of mpa_{dom}_attention alone (no append) between "
+               f"one event pair on its stream, after {how_alone[dom][1]} untimed launches (at least 25 ms)",
     }
     total_bytes = work["decode_bytes"] + work["prefill_bytes"] + work["append_bytes"]
     total_flops = work["decode_flops"] + work["prefill_flops"]
