@@ -45,6 +45,20 @@ int check_shape(const mpa_shape* sh) {
   return MPA_OK;
 }
 
+// The MFMA prefill launch's work units (query tiles x KV heads) over the
+// chunks, and the most KV splits any chunk's prefix allows.
+void prefill_units(const mpa_shape* sh, const std::vector<int>& prefill, const int32_t* seq_lens,
+                   const int32_t* qsl, long* units, int* most) {
+  const int qt = mpa::kPrefillRowsMfma / (sh->num_q_heads / sh->num_kv_heads);
+  *units = 0;
+  *most = 1;
+  for (int s : prefill) {
+    const int C = qsl[s + 1] - qsl[s];
+    *units += (long)(C + qt - 1) / qt * sh->num_kv_heads;
+    *most = std::max(*most, std::min(1 + (seq_lens[s] - C) / 64 / mpa::kPrefillMinSplitTiles, 64));
+  }
+}
+
 // Whether the planner leaves every prefill chunk of the batch whole (one KV
 // split each): f32 chunks, and MFMA batches with at least two workgroups
 // per CU or no prefix long enough to split, unless MPA_PREFILL_SPLITS
@@ -56,14 +70,9 @@ bool prefill_whole(const mpa_shape* sh, const std::vector<int>& prefill, const i
     const int v = atoi(env);
     if (v >= 1 && v <= 64) return false;
   }
-  const int qt = mpa::kPrefillRowsMfma / (sh->num_q_heads / sh->num_kv_heads);
-  long units = 0;
-  int most = 1;  // the most splits any chunk can take
-  for (int s : prefill) {
-    const int C = qsl[s + 1] - qsl[s];
-    units += (long)(C + qt - 1) / qt * sh->num_kv_heads;
-    most = std::max(most, std::min(1 + (seq_lens[s] - C) / 64 / mpa::kPrefillMinSplitTiles, 64));
-  }
+  long units;
+  int most;
+  prefill_units(sh, prefill, seq_lens, qsl, &units, &most);
   return units >= 2L * mpa::kPrefillSplitTarget || most == 1;
 }
 
@@ -328,14 +337,9 @@ std::vector<PrefillSplit> prefill_splits(const mpa_shape* sh, const Batch& b, co
     if (v >= 1 && v <= 64) return split_layout(b, seq_lens, qsl, v, first_item);
   }
   if (prefill_whole(sh, b.prefill, seq_lens, qsl)) return std::vector<PrefillSplit>(b.prefill.size());
-  const int qt = q_tile(sh);
-  long units = 0;
-  int most = 1;  // the most splits any chunk can take
-  for (int s : b.prefill) {
-    const int C = qsl[s + 1] - qsl[s];
-    units += (long)(C + qt - 1) / qt * sh->num_kv_heads;
-    most = std::max(most, std::min(1 + (seq_lens[s] - C) / 64 / mpa::kPrefillMinSplitTiles, 64));
-  }
+  long units;
+  int most;  // the most splits any chunk can take
+  prefill_units(sh, b.prefill, seq_lens, qsl, &units, &most);
   PlanMemo& m = plan_memo(sh, seq_lens, qsl);
   if (m.want == 0) {
     double best_t = -1.0;
